@@ -1,0 +1,198 @@
+"""Benchmark: bounded KV-window recomputation on one MI355X.
+
+One step = one crf_recompute_window call over the 7B-shaped workload: 16384
+prefix tokens re-run through decoder layers [14, 16) (Qwen2.5-7B shapes,
+rank-16 LoRA on all seven projections, paged bf16 KV cache with 16-token
+pages), inputs resident in HBM before the timed region.  Prints one JSON line.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "recomputed token-layers/sec and ms per 16K-token window (7B-shape); MFMA util"
+PEAK_BF16 = 2.5e15      # MI355X dense bf16 MFMA, FLOP/s
+PEAK_HBM = 8.0e12       # bytes/s
+
+
+def window_flops(dims, n, h, rank, targets):
+    """Algorithmic FLOP of one window (causal attention counts only q <= p)."""
+    d, dq, dkv, f = dims.d_model, dims.dq, dims.dkv, dims.d_ffn
+    gemm = 2 * n * (d * (dq + 2 * dkv) + dq * d + d * 2 * f + f * d)
+    lora = 0
+    for t in targets:
+        d_out, d_in = dims.target_shape(t)
+        lora += 2 * n * rank * (d_in + d_out)
+    attn = 2 * 2 * dims.n_q_heads * dims.head_dim * (n * (n + 1) // 2)
+    return h * (gemm + lora + attn), {"gemm": gemm, "lora": lora, "attn": attn}
+
+
+def kernel_flops(dims, n, rank, targets):
+    """Algorithmic FLOP per launch of the projection kernels (base GEMM plus the
+    in-kernel LoRA up-projection) and of the attention kernel."""
+    d, dq, dkv, f = dims.d_model, dims.dq, dims.dkv, dims.d_ffn
+
+    def up(ts):
+        return sum(2 * n * rank * dims.target_shape(t)[0] for t in ts if t in targets)
+    return {
+        "gemm_qkv": 2 * n * d * (dq + 2 * dkv) + up(("q", "k", "v")),
+        "gemm_o": 2 * n * dq * d + up(("o",)),
+        "gemm_gateup": 2 * n * d * 2 * f + up(("gate", "up")),
+        "gemm_down": 2 * n * f * d + up(("down",)),
+        "attn": 2 * 2 * dims.n_q_heads * dims.head_dim * (n * (n + 1) // 2),
+    }
+
+
+def cpu_baseline(case, n_sample: int):
+    """The oracle (fp64 numpy) on the first n_sample prefix tokens of the same
+    window; returns token-layers/s, seconds and thread count."""
+    import numpy as np
+    from oracle import oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+    except Exception:
+        threads = len(os.sched_getaffinity(0))
+    win = case.window
+    h0 = case.hidden[:n_sample]
+    t0 = time.perf_counter()
+    O.recompute_window(h0, case.weights, case.lora, win.l0, win.h, case.dims, case.wl.lora_scale)
+    dt = time.perf_counter() - t0
+    return n_sample * win.h / dt, dt, threads
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="qwen7b_16k")
+    ap.add_argument("--seed", type=int, default=7)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-tokens", type=int, default=8192)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only: the recomputation path is built and measured on a single MI355X "
+              f"(--gpus {args.gpus} is not supported; see DESIGN.md for how it would shard).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2609_30884_amd as crf
+    import synthetic as syn
+    from synthetic.device import build_case
+
+    crf.load()
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    wl = syn.WORKLOADS[args.workload]
+    dims = wl.dims
+    win = wl.window
+    keep_host = not args.no_cpu_baseline
+    t_gen = time.perf_counter()
+    case = build_case(wl, args.seed, keep_host=keep_host)
+    torch.cuda.synchronize()
+    t_gen = time.perf_counter() - t_gen
+    print(f"[bench] inputs ready in {t_gen:.1f}s: {wl.name} n={win.n_tokens} window=[{win.l0},{win.l0 + win.h})",
+          file=sys.stderr, flush=True)
+
+    cd = crf.make_dims(dims.n_layers, dims.d_model, dims.n_q_heads, dims.n_kv_heads, dims.head_dim, dims.d_ffn,
+                       dims.rms_eps, dims.rope_theta, dims.dtype)
+    ctx = crf.Context(cd, win.n_tokens, wl.lora_rank)
+    weights = crf.layer_weights_array(case.weights_dev)
+    lora = crf.lora_array(case.lora_dev, dims.n_layers)
+    kv = crf.kv_cache(case.k_pool, case.v_pool, case.block_table_dev, win.n_tokens, wl.page_size)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        crf.recompute_window(ctx, cd, case.hidden_dev, weights, lora, win.l0, win.h, kv, case.hidden_out, stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    ctx.set_timing(True)
+    ctx.read_timing()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ctx.set_timing(False)
+    timing = ctx.read_timing()
+    flags = ctx.device_errors()
+    assert flags == 0, f"device error flags {flags}"
+
+    ms = 1e3 * elapsed / args.steps
+    tl_per_s = win.n_tokens * win.h * args.steps / elapsed
+    f_win, f_parts = window_flops(dims, win.n_tokens, win.h, wl.lora_rank, wl.lora_targets)
+    kflops = kernel_flops(dims, win.n_tokens, wl.lora_rank, wl.lora_targets)
+    kernels = {}
+    for k, (tot_ms, cnt) in timing.items():
+        if cnt:
+            avg = tot_ms / cnt
+            e = {"avg_ms": round(avg, 4), "launches": cnt, "share": round(tot_ms / (ms * args.steps), 4)}
+            if k in kflops:
+                e["tflops"] = round(kflops[k] / (avg * 1e-3) / 1e12, 1)
+            kernels[k] = e
+    dom = max((k for k in kernels if k in kflops), key=lambda k: timing[k][0])
+    dom_avg_s = timing[dom][0] / timing[dom][1] * 1e-3
+    achieved = kflops[dom] / dom_avg_s
+    traffic = None
+    prof = os.path.join(ROOT, "profiles", f"traffic_{dom}_{wl.name}.json")
+    if os.path.exists(prof):
+        try:
+            traffic = json.load(open(prof)).get("bytes_per_launch")
+        except Exception:
+            traffic = None
+
+    out = {
+        "metric": METRIC,
+        "value": round(tl_per_s, 1),
+        "unit": "token-layers/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if dims.dtype == "bf16" else "f32",
+        "data": "synthetic (seeded N(0,1) boundary state, random-init N(0,0.02) weights, LoRA A~N(0,1/8), "
+                "B~N(0,0.01)+N(0,0.005)); no dataset or checkpoint",
+        "config": {
+            "workload": f"{wl.name}: Qwen2.5-7B-shaped bounded window, {win.n_tokens}-token prefix, layers "
+                        f"[{win.l0},{win.l0 + win.h}) of {dims.n_layers}, LoRA rank {wl.lora_rank} on "
+                        f"{','.join(wl.lora_targets)}, paged KV {wl.page_size}-token pages",
+            "n_tokens": win.n_tokens, "l0": win.l0, "h": win.h, "d_model": dims.d_model, "n_q_heads": dims.n_q_heads,
+            "n_kv_heads": dims.n_kv_heads, "head_dim": dims.head_dim, "d_ffn": dims.d_ffn, "lora_rank": wl.lora_rank,
+        },
+        "mfma_util": round(f_win / (elapsed / args.steps) / PEAK_BF16, 4),
+        "window_tflops": round(f_win / (elapsed / args.steps) / 1e12, 1),
+        "roofline": {"bound": "mfma", "kernel": dom, "achieved": round(achieved / 1e12, 1),
+                     "peak": PEAK_BF16 / 1e12, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16, 4),
+                     "traffic": traffic},
+        "kernels": kernels,
+    }
+    if not args.no_cpu_baseline:
+        ns = min(args.cpu_sample_tokens, win.n_tokens)
+        print(f"[bench] cpu baseline: oracle on {ns} tokens ...", file=sys.stderr, flush=True)
+        v, dt, thr = cpu_baseline(case, ns)
+        out["cpu_baseline"] = {
+            "value": round(v, 1), "unit": "token-layers/s", "cores": thr, "kind": "oracle",
+            "sample": f"fp64 numpy oracle, first {ns} of {win.n_tokens} prefix tokens through layers "
+                      f"[{win.l0},{win.l0 + win.h}) ({dt:.1f} s; causal attention over that shorter prefix)",
+        }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

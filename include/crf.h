@@ -1,0 +1,230 @@
+/*
+ * crf.h — C ABI of the bounded stale-KV recomputation library (libcrf.so).
+ *
+ * The library implements the recovery executor of CacheReforge
+ * (arxiv 2609.30884): when an evolving LoRA adapter has moved on from the
+ * version that produced a KV cache, a contiguous window of decoder layers
+ * [l0, l0+h) is re-run over the complete cached prefix under the current
+ * adapter, starting from the hidden state retained at the restart boundary,
+ * and the refreshed K/V overwrite those layers' slots of the cache
+ * (paper Sec. 4.2 "Executable restart"; supplementary Sec. S1.1, definition of
+ * the operation R_{r,h}).  It also scores the per-layer adapter drift and risk
+ * that feed the reuse / bounded / full-suffix choice (Sec. 4.1, Eq. 8); that
+ * choice itself stays with the caller.
+ *
+ * General conventions
+ *   - Every tensor pointer is a DEVICE pointer on the current HIP device,
+ *     allocated and owned by the caller.  The library owns only the workspace
+ *     inside a crf_context.  Host arrays (per-layer descriptor arrays, the
+ *     anchor index array) are read during the call only.
+ *   - Tensors are dense row-major.  Weights use the nn.Linear layout
+ *     [d_out, d_in].  The storage type of every floating-point tensor is
+ *     crf_model_dims.dtype (fp32 or bf16); accumulation is always fp32.
+ *   - bf16 tensors must be 16-byte aligned; fp32 tensors 16-byte aligned.
+ *   - Work is enqueued asynchronously on `stream` (a hipStream_t; NULL is the
+ *     default stream).  No call synchronises the device except where stated.
+ *   - Errors are returned as crf_status codes, never by aborting.  Shape,
+ *     range and pointer checks happen on the host before anything is
+ *     launched; a failed check launches nothing.  The message of the last
+ *     failure is available from crf_last_error().
+ *   - A context is not thread-safe; use one context per stream.  Calls that
+ *     overlap on one context race on its workspace.
+ */
+#ifndef CRF_H
+#define CRF_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define CRF_ABI_VERSION 1
+
+typedef enum {
+  CRF_OK = 0,
+  CRF_ERR_INVALID_ARG = 1,  /* null pointer, misaligned pointer, bad enum      */
+  CRF_ERR_SHAPE = 2,        /* tensor/cache sizes inconsistent                  */
+  CRF_ERR_RANGE = 3,        /* layer window outside [0, n_layers)              */
+  CRF_ERR_UNSUPPORTED = 4,  /* valid model but not a shape this build handles   */
+  CRF_ERR_WORKSPACE = 5,    /* exceeds the context's max_tokens / max rank     */
+  CRF_ERR_HIP = 6,          /* a HIP runtime call failed                        */
+  CRF_ERR_DEVICE = 7        /* a kernel's own bounds check fired (see below)   */
+} crf_status;
+
+typedef enum { CRF_F32 = 0, CRF_BF16 = 1 } crf_dtype;
+
+/* Projection targets of one decoder layer (supplementary Eq. sup-qkv-current-layer
+ * names Q, K, V; the output and MLP projections are the remaining update
+ * targets of supplementary Eq. sup-first-invalid-cache-layer). */
+enum { CRF_Q = 0, CRF_K, CRF_V, CRF_O, CRF_GATE, CRF_UP, CRF_DOWN, CRF_NUM_TARGETS };
+
+/* Decoder shape.  Layers are indexed 0..n_layers-1 (Sec. 2.2, Eq. 1).
+ * Target shapes: q [n_q_heads*head_dim, d_model], k and v
+ * [n_kv_heads*head_dim, d_model], o [d_model, n_q_heads*head_dim],
+ * gate and up [d_ffn, d_model], down [d_model, d_ffn]. */
+typedef struct {
+  int32_t n_layers, d_model, n_q_heads, n_kv_heads, head_dim, d_ffn;
+  float rms_eps;      /* RMSNorm epsilon, inside the square root          */
+  float rope_theta;   /* rotary base: angle(p, i) = p * theta^(-2i/hd)     */
+  int32_t dtype;      /* crf_dtype: storage type of every tensor          */
+} crf_model_dims;
+
+/* Frozen base weights of one layer.  attn_norm, mlp_norm: RMSNorm gains [d_model].
+ * w[t]: [d_out, d_in] of target t.  bias_q/k/v: optional [d_out] (NULL = none). */
+typedef struct {
+  const void *attn_norm, *mlp_norm;
+  const void *w[CRF_NUM_TARGETS];
+  const void *bias_q, *bias_k, *bias_v;
+} crf_layer_weights;
+
+/* Current LoRA adapter state of one layer: delta_t(x) = scale * (x A_t^T) B_t^T
+ * with A_t [rank, d_in] and B_t [d_out, rank].  A[t] == NULL (with B[t] == NULL)
+ * means target t carries no adapter.  rank 0 means the layer has no adapter. */
+typedef struct {
+  int32_t rank;
+  float scale;
+  const void *A[CRF_NUM_TARGETS];
+  const void *B[CRF_NUM_TARGETS];
+} crf_lora_layer;
+
+/* Paged layerwise KV cache C = {K_l, V_l} (Sec. 2.2, Eq. 1).
+ * k_pool / v_pool element (layer, page, kv_head, slot, e) lives at
+ *   layer*layer_stride + page*page_stride + (kv_head*page_size + slot)*head_dim + e
+ * (strides in elements).  Logical token t lives in physical page
+ * block_table[t / page_size] (a DEVICE int32 array of ceil(n_tokens/page_size)
+ * entries, shared by all layers), slot t % page_size.  K is stored after the
+ * rotary rotation, V unrotated.  Pages not named by the block table, slots
+ * past n_tokens and layers outside the window are never written.  A block
+ * table entry outside [0, n_pages) is caught by the kernels: they skip that
+ * page (treating its keys/values as zero) and raise the context's device
+ * error flag (crf_context_device_errors). */
+typedef struct {
+  void *k_pool, *v_pool;
+  int64_t layer_stride, page_stride;
+  const int32_t *block_table;
+  int32_t n_pages, page_size, n_tokens;
+} crf_kv_cache;
+
+typedef struct crf_context crf_context;
+
+/* Kernel classes for the optional event timing (crf_context_set_timing). */
+enum {
+  CRF_KK_NORM = 0, CRF_KK_LORA_DOWN, CRF_KK_GEMM_QKV, CRF_KK_ATTN, CRF_KK_GEMM_O,
+  CRF_KK_GEMM_GATEUP, CRF_KK_GEMM_DOWN, CRF_KK_DRIFT, CRF_KK_OTHER, CRF_KK_COUNT
+};
+
+/* Human-readable name of a status code (static string). */
+const char *crf_status_string(crf_status s);
+
+/* ABI version of the loaded library (CRF_ABI_VERSION at build time). */
+int32_t crf_abi_version(void);
+
+/* Create a context for `dims` on the current HIP device.  Allocates the
+ * workspace for windows of up to max_tokens prefix tokens and LoRA ranks up
+ * to max_lora_rank, and the rotary angle table for positions
+ * 0..max_tokens-1.  On success *out receives the context (destroy with
+ * crf_context_destroy).  Errors: INVALID_ARG (null), UNSUPPORTED (see
+ * crf_validate_dims), HIP (allocation failed). */
+crf_status crf_context_create(const crf_model_dims *dims, int32_t max_tokens, int32_t max_lora_rank,
+                              crf_context **out);
+void crf_context_destroy(crf_context *ctx);
+
+/* Message of the last failure on this context ("" if none).  With ctx == NULL,
+ * the message of the last failure of a call made without a context. */
+const char *crf_last_error(const crf_context *ctx);
+
+/* Host-only check of a decoder shape: every dimension positive,
+ * n_q_heads % n_kv_heads == 0, head_dim in {64, 128}, and for bf16 the
+ * projection widths multiples of 128 and d_ffn a multiple of 64.  Touches no
+ * device.  Errors: INVALID_ARG, SHAPE, UNSUPPORTED. */
+crf_status crf_validate_dims(const crf_model_dims *dims);
+
+/* Host-only check of a recomputation request (Sec. 4.1: the candidate window
+ * min(h, N - r) never passes the last layer; supplementary terminology table:
+ * ranges are half-open).  Checks dims as above, 0 <= l0, 0 <= h,
+ * l0 + h <= n_layers (else RANGE), and the cache geometry: page_size >= 1,
+ * n_tokens >= 0, n_tokens <= n_pages * page_size, page_stride >=
+ * n_kv_heads*page_size*head_dim, layer_stride >= n_pages*page_stride (else
+ * SHAPE), non-null pools and block table when h > 0 and n_tokens > 0 (else
+ * INVALID_ARG).  Touches no device. */
+crf_status crf_validate_window(const crf_model_dims *dims, int32_t l0, int32_t h, const crf_kv_cache *kv);
+
+/* Bounded recomputation R_{l0,h} (Sec. 4.2 "Executable restart"; supplementary
+ * Sec. S1.1): starting from hidden_at_boundary = H_{l0-1} [n_tokens, d_model]
+ * (the residual-stream output of layer l0-1, or the embedding state H_{-1}
+ * when l0 == 0), run decoder layers l0..l0+h-1 over all n_tokens prefix
+ * tokens under the current adapter `lora`, and overwrite layer l's K/V slots
+ * of `kv_cache` for every l in the window with the recomputed, rotated K and
+ * V.  Each layer: RMSNorm, Q/K/V projections with the LoRA delta, rotary
+ * rotation of Q and K at positions 0..n_tokens-1, causal grouped-query
+ * softmax attention (query head j reads K/V head j / (n_q_heads/n_kv_heads),
+ * scale 1/sqrt(head_dim)), output projection with LoRA delta and residual,
+ * RMSNorm, SwiGLU MLP down(silu(gate x) * up x) with LoRA deltas and residual.
+ *   base_weights: host array [n_layers]; only the window's entries are read.
+ *   lora:         host array [n_layers] of the current adapter, or NULL (no adapter).
+ *   hidden_out:   [n_tokens, d_model] receives H_{l0+h-1}; may be NULL; may alias
+ *                 hidden_at_boundary.
+ * h == 0 is direct reuse: nothing is launched and hidden_out (if given and
+ * distinct) is not written.  Layers outside the window and pages outside the
+ * block table are never touched.  n_tokens comes from kv_cache->n_tokens and
+ * must not exceed the context's max_tokens (else WORKSPACE).
+ * Errors: as crf_validate_window, plus INVALID_ARG (null or misaligned
+ * weights/boundary, dims differing from the context's), WORKSPACE, HIP. */
+crf_status crf_recompute_window(crf_context *ctx, const crf_model_dims *dims, const void *hidden_at_boundary,
+                                const crf_layer_weights *base_weights, const crf_lora_layer *lora, int32_t l0,
+                                int32_t h, const crf_kv_cache *kv_cache, void *hidden_out, void *stream);
+
+/* One stale cache of a batched request. */
+typedef struct {
+  const void *hidden_at_boundary;   /* [kv.n_tokens, d_model] = H_{l0-1}          */
+  const crf_lora_layer *lora;       /* host array [n_layers] or NULL              */
+  int32_t l0, h;
+  crf_kv_cache kv;
+  void *hidden_out;                 /* [kv.n_tokens, d_model] or NULL             */
+} crf_window_item;
+
+/* crf_recompute_window over several independent stale caches of one base
+ * model, each with its own boundary state, window and adapter version (the
+ * per-cache decision of Sec. 4.1 applied to many caches at once).  Every item
+ * is validated before anything is launched; items run in order on `stream`.
+ * Errors: as crf_recompute_window; the failing item's index is in the message. */
+crf_status crf_recompute_window_batched(crf_context *ctx, const crf_model_dims *dims,
+                                        const crf_layer_weights *base_weights, int32_t n_items,
+                                        const crf_window_item *items, void *stream);
+
+/* Runtime drift and risk (Sec. 4.1 "Runtime risk and range selection", Eq. 8):
+ *   d_l = || theta_t - theta_l^anchor ||_2,   q_l = s_l * d_l.
+ * theta is the whole adapter: every A and B entry of every target of every
+ * layer.  current: host array [n_layers] (theta_t).  versions: host array of
+ * n_versions pointers, each to a host array [n_layers] of stored adapter
+ * states; anchor_version: host int32 [n_layers], index of the version that
+ * produced layer l's cache.  Targets present in `current` must be present
+ * with the same rank in every version.  sensitivity: device fp32 [n_layers]
+ * (s_l) or NULL for s = 1.  per_layer_only != 0 restricts the norm to layer
+ * l's own slice.  Outputs (device fp32): drift_out [n_layers], risk_out
+ * [n_layers], sq_partial_out [n_versions * n_layers] (squared distance of
+ * layer l's slice to version v at index v*n_layers + l; may be NULL).
+ * Errors: INVALID_ARG (null, anchor index out of range, target missing in a
+ * version), SHAPE, HIP. */
+crf_status crf_layer_drift(crf_context *ctx, const crf_model_dims *dims, const crf_lora_layer *current,
+                           int32_t n_versions, const crf_lora_layer *const *versions,
+                           const int32_t *anchor_version, const float *sensitivity, int32_t per_layer_only,
+                           float *drift_out, float *risk_out, float *sq_partial_out, void *stream);
+
+/* Device-side error flags raised by kernels' own bounds checks since the last
+ * call (bit 0: a block table entry outside [0, n_pages)).  Synchronises the
+ * device, then clears the flags. */
+crf_status crf_context_device_errors(crf_context *ctx, int32_t *flags_out);
+
+/* Optional per-kernel-class event timing.  While enabled, each launch is
+ * bracketed by HIP events on its stream.  crf_context_read_timing
+ * synchronises those events and returns, per kernel class (CRF_KK_*), the
+ * summed milliseconds and launch counts since the last read, then resets. */
+crf_status crf_context_set_timing(crf_context *ctx, int32_t enable);
+crf_status crf_context_read_timing(crf_context *ctx, float *ms_out, int32_t *count_out, int32_t n_kinds);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* CRF_H */

@@ -1,0 +1,677 @@
+// Host side of the C ABI (include/crf.h): validation, workspace, launch order.
+#include <hip/hip_runtime.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+#include <initializer_list>
+#include <string>
+#include <vector>
+
+#include "../../include/crf.h"
+#include "kernels.hpp"
+
+using namespace crf;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+struct Timer {
+  bool on = false;
+  std::vector<hipEvent_t> ev;   // pairs (start, stop)
+  std::vector<int> kind;        // per pair
+  size_t used = 0;              // pairs recorded since last read
+};
+
+}  // namespace
+
+struct crf_context {
+  crf_model_dims dims;
+  int32_t max_tokens = 0, max_rank = 0, rank_pad = 0;
+  int device = 0;
+  size_t esz = 2;
+  // workspace
+  float *hres = nullptr;   // [T, d] residual stream, fp32
+  void *xn = nullptr;      // [T, d] normalised input
+  void *q = nullptr;       // [T, dq] rotated queries
+  void *attn = nullptr;    // [T, dq] attention output
+  void *act = nullptr;     // [T, f] SwiGLU output
+  void *u = nullptr;       // bf16: [T, 3*rank_pad] LoRA down-projections; fp32: [T, max_rank]
+  float *proj = nullptr;   // fp32 path: [T, dq + 2 dkv]
+  float *gu = nullptr;     // fp32 path: [T, 2f]
+  float2 *rope_cs = nullptr;
+  int *d_err = nullptr;
+  // drift staging
+  void *drift_host = nullptr;
+  size_t drift_host_bytes = 0;
+  void *drift_dev = nullptr;
+  size_t drift_dev_bytes = 0;
+  hipEvent_t drift_ev = nullptr;
+  bool drift_ev_recorded = false;
+  std::string last_error;
+  Timer timer;
+};
+
+namespace {
+
+crf_status fail(crf_context *ctx, crf_status st, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  if (ctx)
+    ctx->last_error = buf;
+  else
+    g_last_error = buf;
+  return st;
+}
+
+#define HIP_TRY(ctx, expr)                                                                       \
+  do {                                                                                           \
+    hipError_t e_ = (expr);                                                                      \
+    if (e_ != hipSuccess) return fail(ctx, CRF_ERR_HIP, "%s: %s", #expr, hipGetErrorString(e_)); \
+  } while (0)
+
+bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+
+int dq_of(const crf_model_dims &d) { return d.n_q_heads * d.head_dim; }
+int dkv_of(const crf_model_dims &d) { return d.n_kv_heads * d.head_dim; }
+
+void target_shape(const crf_model_dims &d, int t, int &d_out, int &d_in) {
+  const int dq = dq_of(d), dkv = dkv_of(d);
+  switch (t) {
+    case CRF_Q: d_out = dq; d_in = d.d_model; break;
+    case CRF_K: case CRF_V: d_out = dkv; d_in = d.d_model; break;
+    case CRF_O: d_out = d.d_model; d_in = dq; break;
+    case CRF_GATE: case CRF_UP: d_out = d.d_ffn; d_in = d.d_model; break;
+    default: d_out = d.d_model; d_in = d.d_ffn; break;
+  }
+}
+
+crf_status check_dims(crf_context *ctx, const crf_model_dims *d) {
+  if (!d) return fail(ctx, CRF_ERR_INVALID_ARG, "dims is NULL");
+  if (d->n_layers <= 0 || d->d_model <= 0 || d->n_q_heads <= 0 || d->n_kv_heads <= 0 || d->head_dim <= 0 ||
+      d->d_ffn <= 0)
+    return fail(ctx, CRF_ERR_SHAPE, "every model dimension must be positive");
+  if (!(d->rms_eps >= 0.f) || !(d->rope_theta > 0.f))
+    return fail(ctx, CRF_ERR_SHAPE, "rms_eps must be >= 0 and rope_theta > 0");
+  if (d->dtype != CRF_F32 && d->dtype != CRF_BF16) return fail(ctx, CRF_ERR_INVALID_ARG, "unknown dtype %d", d->dtype);
+  if (d->n_q_heads % d->n_kv_heads)
+    return fail(ctx, CRF_ERR_UNSUPPORTED, "n_q_heads (%d) must be a multiple of n_kv_heads (%d)", d->n_q_heads,
+                d->n_kv_heads);
+  if (d->head_dim != 64 && d->head_dim != 128)
+    return fail(ctx, CRF_ERR_UNSUPPORTED, "head_dim %d not in {64, 128}", d->head_dim);
+  if (d->d_model % 8 || d->d_ffn % 8)
+    return fail(ctx, CRF_ERR_UNSUPPORTED, "d_model and d_ffn must be multiples of 8");
+  if (d->dtype == CRF_BF16) {
+    if (d->d_model % 128 || dq_of(*d) % 128 || dkv_of(*d) % 128 || d->d_ffn % 64)
+      return fail(ctx, CRF_ERR_UNSUPPORTED,
+                  "bf16 path needs d_model, n_q_heads*head_dim, n_kv_heads*head_dim multiples of 128 and d_ffn a "
+                  "multiple of 64");
+  }
+  return CRF_OK;
+}
+
+crf_status check_window(crf_context *ctx, const crf_model_dims *d, int32_t l0, int32_t h, const crf_kv_cache *kv) {
+  crf_status st = check_dims(ctx, d);
+  if (st != CRF_OK) return st;
+  if (l0 < 0 || h < 0 || (int64_t)l0 + h > d->n_layers)
+    return fail(ctx, CRF_ERR_RANGE, "window [%d, %d+%d) outside [0, %d)", l0, l0, h, d->n_layers);
+  if (!kv) return fail(ctx, CRF_ERR_INVALID_ARG, "kv_cache is NULL");
+  if (kv->page_size < 1 || kv->n_pages < 0 || kv->n_tokens < 0)
+    return fail(ctx, CRF_ERR_SHAPE, "page_size must be >= 1, n_pages and n_tokens >= 0");
+  if ((int64_t)kv->n_tokens > (int64_t)kv->n_pages * kv->page_size)
+    return fail(ctx, CRF_ERR_SHAPE, "n_tokens %d exceeds n_pages*page_size = %lld", kv->n_tokens,
+                (long long)kv->n_pages * kv->page_size);
+  if (kv->page_stride < (int64_t)d->n_kv_heads * kv->page_size * d->head_dim)
+    return fail(ctx, CRF_ERR_SHAPE, "page_stride %lld < n_kv_heads*page_size*head_dim", (long long)kv->page_stride);
+  if (kv->layer_stride < (int64_t)kv->n_pages * kv->page_stride)
+    return fail(ctx, CRF_ERR_SHAPE, "layer_stride %lld < n_pages*page_stride", (long long)kv->layer_stride);
+  if (h > 0 && kv->n_tokens > 0 && (!kv->k_pool || !kv->v_pool || !kv->block_table))
+    return fail(ctx, CRF_ERR_INVALID_ARG, "k_pool, v_pool and block_table must be non-NULL");
+  return CRF_OK;
+}
+
+bool same_dims(const crf_model_dims &a, const crf_model_dims &b) {
+  return a.n_layers == b.n_layers && a.d_model == b.d_model && a.n_q_heads == b.n_q_heads &&
+         a.n_kv_heads == b.n_kv_heads && a.head_dim == b.head_dim && a.d_ffn == b.d_ffn && a.rms_eps == b.rms_eps &&
+         a.rope_theta == b.rope_theta && a.dtype == b.dtype;
+}
+
+// Full validation of one window request against a context (host only).
+crf_status check_request(crf_context *ctx, const crf_model_dims *dims, const void *hb,
+                         const crf_layer_weights *w, const crf_lora_layer *lora, int32_t l0, int32_t h,
+                         const crf_kv_cache *kv, const void *hout, const char *what) {
+  crf_status st = check_window(ctx, dims, l0, h, kv);
+  if (st != CRF_OK) return st;
+  if (!same_dims(*dims, ctx->dims)) return fail(ctx, CRF_ERR_INVALID_ARG, "%s: dims differ from the context's", what);
+  if (h == 0 || kv->n_tokens == 0) return CRF_OK;
+  if (kv->n_tokens > ctx->max_tokens)
+    return fail(ctx, CRF_ERR_WORKSPACE, "%s: n_tokens %d exceeds the context's max_tokens %d", what, kv->n_tokens,
+                ctx->max_tokens);
+  if (!hb || !aligned16(hb)) return fail(ctx, CRF_ERR_INVALID_ARG, "%s: hidden_at_boundary NULL or misaligned", what);
+  if (hout && !aligned16(hout)) return fail(ctx, CRF_ERR_INVALID_ARG, "%s: hidden_out misaligned", what);
+  if (!aligned16(kv->k_pool) || !aligned16(kv->v_pool) || kv->page_stride % 8 || kv->layer_stride % 8)
+    return fail(ctx, CRF_ERR_INVALID_ARG, "%s: KV pools must be 16-byte aligned with strides multiple of 8", what);
+  if (!w) return fail(ctx, CRF_ERR_INVALID_ARG, "%s: base_weights is NULL", what);
+  for (int l = l0; l < l0 + h; ++l) {
+    const crf_layer_weights &lw = w[l];
+    if (!lw.attn_norm || !lw.mlp_norm || !aligned16(lw.attn_norm) || !aligned16(lw.mlp_norm))
+      return fail(ctx, CRF_ERR_INVALID_ARG, "%s: layer %d norm gains NULL or misaligned", what, l);
+    for (int t = 0; t < CRF_NUM_TARGETS; ++t)
+      if (!lw.w[t] || !aligned16(lw.w[t]))
+        return fail(ctx, CRF_ERR_INVALID_ARG, "%s: layer %d weight %d NULL or misaligned", what, l, t);
+    if (lora) {
+      const crf_lora_layer &ll = lora[l];
+      if (ll.rank < 0) return fail(ctx, CRF_ERR_INVALID_ARG, "%s: layer %d negative LoRA rank", what, l);
+      if (ll.rank > ctx->max_rank)
+        return fail(ctx, CRF_ERR_WORKSPACE, "%s: layer %d LoRA rank %d exceeds the context's %d", what, l, ll.rank,
+                    ctx->max_rank);
+      if (ll.rank > 0 && ctx->dims.dtype == CRF_BF16 && ll.rank % 8)
+        return fail(ctx, CRF_ERR_UNSUPPORTED, "%s: bf16 path needs LoRA rank multiple of 8 (got %d)", what, ll.rank);
+      for (int t = 0; t < CRF_NUM_TARGETS && ll.rank > 0; ++t) {
+        if ((ll.A[t] == nullptr) != (ll.B[t] == nullptr))
+          return fail(ctx, CRF_ERR_INVALID_ARG, "%s: layer %d target %d has only one LoRA factor", what, l, t);
+        if (ll.A[t] && (!aligned16(ll.A[t]) || !aligned16(ll.B[t])))
+          return fail(ctx, CRF_ERR_INVALID_ARG, "%s: layer %d target %d LoRA factor misaligned", what, l, t);
+      }
+    }
+  }
+  return CRF_OK;
+}
+
+// ----------------------------------------------------------------------------- timing
+
+struct Launch {
+  crf_context *ctx;
+  hipStream_t s;
+  int kind;
+  size_t idx = 0;
+  Launch(crf_context *c, hipStream_t st, int k) : ctx(c), s(st), kind(k) {
+    Timer &t = ctx->timer;
+    if (!t.on) return;
+    idx = t.used;
+    if (2 * idx + 2 > t.ev.size()) {
+      hipEvent_t a, b;
+      if (hipEventCreate(&a) != hipSuccess || hipEventCreate(&b) != hipSuccess) return;
+      t.ev.push_back(a);
+      t.ev.push_back(b);
+      t.kind.push_back(k);
+    }
+    t.kind[idx] = k;
+    (void)hipEventRecord(t.ev[2 * idx], s);
+  }
+  ~Launch() {
+    Timer &t = ctx->timer;
+    if (!t.on || 2 * idx + 2 > t.ev.size()) return;
+    (void)hipEventRecord(t.ev[2 * idx + 1], s);
+    t.used = idx + 1;
+  }
+};
+
+#define LAUNCH(ctx, s, kind, expr)                                                                     \
+  do {                                                                                                 \
+    Launch lt_(ctx, s, kind);                                                                          \
+    hipError_t e_ = (expr);                                                                            \
+    if (e_ != hipSuccess) return fail(ctx, CRF_ERR_HIP, "launch %s: %s", #expr, hipGetErrorString(e_)); \
+  } while (0)
+
+// ----------------------------------------------------------------------------- layer sequences
+
+PagedKV layer_kv(crf_context *ctx, const crf_kv_cache *kv, int l) {
+  PagedKV p;
+  p.k = (char *)kv->k_pool + (size_t)l * kv->layer_stride * ctx->esz;
+  p.v = (char *)kv->v_pool + (size_t)l * kv->layer_stride * ctx->esz;
+  p.page_stride = kv->page_stride;
+  p.block_table = kv->block_table;
+  p.n_pages = kv->n_pages;
+  p.page_size = kv->page_size;
+  p.n_tokens = kv->n_tokens;
+  p.err = ctx->d_err;
+  return p;
+}
+
+bool has_lora(const crf_lora_layer *lora, int l, int t) {
+  return lora && lora[l].rank > 0 && lora[l].A[t] != nullptr;
+}
+
+crf_status run_layers_bf16(crf_context *ctx, const void *hb, const crf_layer_weights *W,
+                           const crf_lora_layer *lora, int l0, int h, const crf_kv_cache *kv, void *hout,
+                           hipStream_t s) {
+  const crf_model_dims &d = ctx->dims;
+  const int M = kv->n_tokens, D = d.d_model, dq = dq_of(d), dkv = dkv_of(d), f = d.d_ffn, hd = d.head_dim;
+  const int rp = ctx->rank_pad, ldu = 3 * rp;
+  bf16 *xn = (bf16 *)ctx->xn, *q = (bf16 *)ctx->q, *attn = (bf16 *)ctx->attn, *act = (bf16 *)ctx->act;
+  bf16 *u = (bf16 *)ctx->u;
+  for (int l = l0; l < l0 + h; ++l) {
+    const crf_layer_weights &w = W[l];
+    const bool first = l == l0, last = l == l0 + h - 1;
+    const int rank = lora ? lora[l].rank : 0;
+    const float scale = lora ? lora[l].scale : 0.f;
+    auto lora_targets = [&](std::initializer_list<int> ts, LoraDownTarget *out) {
+      int i = 0;
+      bool any = false;
+      for (int t : ts) {
+        const bool on = has_lora(lora, l, t);
+        out[i] = LoraDownTarget{on ? (const bf16 *)lora[l].A[t] : nullptr, rank, scale, i * rp};
+        any |= on;
+        ++i;
+      }
+      return any;
+    };
+    auto base_params = [&](const bf16 *X, int K, int N) {
+      GemmParams p{};
+      p.X = X;
+      p.ldx = K;
+      p.M = M;
+      p.K = K;
+      p.N = N;
+      p.U = nullptr;
+      p.ldu = ldu;
+      p.kpad = rp;
+      p.rank = rank;
+      p.rope_cs = ctx->rope_cs;
+      return p;
+    };
+    LoraDownTarget tg[3];
+
+    // attention block
+    LAUNCH(ctx, s, CRF_KK_NORM,
+           launch_rmsnorm(s, first ? hb : (const void *)ctx->hres, !first, w.attn_norm, false, xn, false,
+                          first ? ctx->hres : nullptr, M, D, d.rms_eps));
+    bool any = lora_targets({CRF_Q, CRF_K, CRF_V}, tg);
+    if (any) LAUNCH(ctx, s, CRF_KK_LORA_DOWN, launch_lora_down_bf16(s, xn, D, M, D, tg, 3, rp, u, ldu));
+    {
+      GemmParams p = base_params(xn, D, dq + 2 * dkv);
+      p.w[0] = (const bf16 *)w.w[CRF_Q];
+      p.w[1] = (const bf16 *)w.w[CRF_K];
+      p.w[2] = (const bf16 *)w.w[CRF_V];
+      p.seg1 = dq;
+      p.seg2 = dq + dkv;
+      if (any) {
+        p.U = u;
+        for (int i = 0; i < 3; ++i) {
+          const int t = CRF_Q + i;
+          p.lb[i] = has_lora(lora, l, t) ? (const bf16 *)lora[l].B[t] : nullptr;
+          p.ucol[i] = i * rp;
+        }
+      }
+      p.bias[0] = (const bf16 *)w.bias_q;
+      p.bias[1] = (const bf16 *)w.bias_k;
+      p.bias[2] = (const bf16 *)w.bias_v;
+      p.q_out = q;
+      p.dq = dq;
+      p.kv = layer_kv(ctx, kv, l);
+      LAUNCH(ctx, s, CRF_KK_GEMM_QKV, launch_gemm_bf16(s, EPI_QKV, hd, p));
+    }
+    LAUNCH(ctx, s, CRF_KK_ATTN, launch_attn_bf16(s, q, layer_kv(ctx, kv, l), attn, M, d.n_q_heads, d.n_kv_heads, hd));
+    any = lora_targets({CRF_O}, tg);
+    if (any) LAUNCH(ctx, s, CRF_KK_LORA_DOWN, launch_lora_down_bf16(s, attn, dq, M, dq, tg, 1, rp, u, ldu));
+    {
+      GemmParams p = base_params(attn, dq, D);
+      p.w[0] = (const bf16 *)w.w[CRF_O];
+      if (any) {
+        p.U = u;
+        p.lb[0] = (const bf16 *)lora[l].B[CRF_O];
+        p.ucol[0] = 0;
+      }
+      p.resid = ctx->hres;
+      p.ldr = D;
+      LAUNCH(ctx, s, CRF_KK_GEMM_O, launch_gemm_bf16(s, EPI_RESID, hd, p));
+    }
+    // MLP block
+    LAUNCH(ctx, s, CRF_KK_NORM,
+           launch_rmsnorm(s, ctx->hres, true, w.mlp_norm, false, xn, false, nullptr, M, D, d.rms_eps));
+    any = lora_targets({CRF_GATE, CRF_UP}, tg);
+    if (any) LAUNCH(ctx, s, CRF_KK_LORA_DOWN, launch_lora_down_bf16(s, xn, D, M, D, tg, 2, rp, u, ldu));
+    {
+      GemmParams p = base_params(xn, D, 2 * f);
+      p.w[0] = (const bf16 *)w.w[CRF_GATE];
+      p.w[1] = (const bf16 *)w.w[CRF_UP];
+      if (any) {
+        p.U = u;
+        p.lb[0] = has_lora(lora, l, CRF_GATE) ? (const bf16 *)lora[l].B[CRF_GATE] : nullptr;
+        p.lb[1] = has_lora(lora, l, CRF_UP) ? (const bf16 *)lora[l].B[CRF_UP] : nullptr;
+        p.ucol[0] = 0;
+        p.ucol[1] = rp;
+      }
+      p.act = act;
+      p.d_ffn = f;
+      LAUNCH(ctx, s, CRF_KK_GEMM_GATEUP, launch_gemm_bf16(s, EPI_SWIGLU, hd, p));
+    }
+    any = lora_targets({CRF_DOWN}, tg);
+    if (any) LAUNCH(ctx, s, CRF_KK_LORA_DOWN, launch_lora_down_bf16(s, act, f, M, f, tg, 1, rp, u, ldu));
+    {
+      GemmParams p = base_params(act, f, D);
+      p.w[0] = (const bf16 *)w.w[CRF_DOWN];
+      if (any) {
+        p.U = u;
+        p.lb[0] = (const bf16 *)lora[l].B[CRF_DOWN];
+        p.ucol[0] = 0;
+      }
+      p.resid = ctx->hres;
+      p.resid_out = (last && hout) ? (bf16 *)hout : nullptr;
+      p.ldr = D;
+      LAUNCH(ctx, s, CRF_KK_GEMM_DOWN, launch_gemm_bf16(s, EPI_RESID, hd, p));
+    }
+  }
+  return CRF_OK;
+}
+
+crf_status run_layers_f32(crf_context *ctx, const void *hb, const crf_layer_weights *W, const crf_lora_layer *lora,
+                          int l0, int h, const crf_kv_cache *kv, void *hout, hipStream_t s) {
+  const crf_model_dims &d = ctx->dims;
+  const int M = kv->n_tokens, D = d.d_model, dq = dq_of(d), dkv = dkv_of(d), f = d.d_ffn, hd = d.head_dim;
+  const int PW = dq + 2 * dkv;
+  float *xn = (float *)ctx->xn, *q = (float *)ctx->q, *attn = (float *)ctx->attn, *act = (float *)ctx->act;
+  float *u = (float *)ctx->u;
+  // y[:, :] (ldc) += x W^T (+ scale (x A^T) B^T)
+  auto proj = [&](int l, int t, const float *x, int K, float *y, int ldc, float beta) -> crf_status {
+    int d_out, d_in;
+    target_shape(d, t, d_out, d_in);
+    const int kind = t <= CRF_V ? CRF_KK_GEMM_QKV
+                   : t == CRF_O ? CRF_KK_GEMM_O
+                   : t == CRF_DOWN ? CRF_KK_GEMM_DOWN : CRF_KK_GEMM_GATEUP;
+    LAUNCH(ctx, s, kind, launch_gemm_f32(s, M, d_out, K, x, K, (const float *)W[l].w[t], K, y, ldc, 1.f, beta));
+    if (has_lora(lora, l, t)) {
+      const int r = lora[l].rank;
+      LAUNCH(ctx, s, CRF_KK_LORA_DOWN,
+             launch_gemm_f32(s, M, r, K, x, K, (const float *)lora[l].A[t], K, u, r, lora[l].scale, 0.f));
+      LAUNCH(ctx, s, kind, launch_gemm_f32(s, M, d_out, r, u, r, (const float *)lora[l].B[t], r, y, ldc, 1.f, 1.f));
+    }
+    return CRF_OK;
+  };
+  crf_status st;
+  for (int l = l0; l < l0 + h; ++l) {
+    const crf_layer_weights &w = W[l];
+    const bool first = l == l0;
+    LAUNCH(ctx, s, CRF_KK_NORM,
+           launch_rmsnorm(s, first ? hb : (const void *)ctx->hres, true, w.attn_norm, true, xn, true,
+                          first ? ctx->hres : nullptr, M, D, d.rms_eps));
+    if ((st = proj(l, CRF_Q, xn, D, ctx->proj, PW, 0.f)) != CRF_OK) return st;
+    if ((st = proj(l, CRF_K, xn, D, ctx->proj + dq, PW, 0.f)) != CRF_OK) return st;
+    if ((st = proj(l, CRF_V, xn, D, ctx->proj + dq + dkv, PW, 0.f)) != CRF_OK) return st;
+    const PagedKV pk = layer_kv(ctx, kv, l);
+    LAUNCH(ctx, s, CRF_KK_OTHER,
+           launch_qkv_post_f32(s, ctx->proj, (const float *)w.bias_q, (const float *)w.bias_k,
+                               (const float *)w.bias_v, q, pk, ctx->rope_cs, M, d.n_q_heads, d.n_kv_heads, hd));
+    LAUNCH(ctx, s, CRF_KK_ATTN, launch_attn_f32(s, q, pk, attn, M, d.n_q_heads, d.n_kv_heads, hd));
+    if ((st = proj(l, CRF_O, attn, dq, ctx->hres, D, 1.f)) != CRF_OK) return st;
+    LAUNCH(ctx, s, CRF_KK_NORM,
+           launch_rmsnorm(s, ctx->hres, true, w.mlp_norm, true, xn, true, nullptr, M, D, d.rms_eps));
+    if ((st = proj(l, CRF_GATE, xn, D, ctx->gu, 2 * f, 0.f)) != CRF_OK) return st;
+    if ((st = proj(l, CRF_UP, xn, D, ctx->gu + f, 2 * f, 0.f)) != CRF_OK) return st;
+    LAUNCH(ctx, s, CRF_KK_OTHER, launch_silu_mul_f32(s, ctx->gu, act, M, f));
+    if ((st = proj(l, CRF_DOWN, act, f, ctx->hres, D, 1.f)) != CRF_OK) return st;
+  }
+  if (hout) HIP_TRY(ctx, hipMemcpyAsync(hout, ctx->hres, (size_t)M * D * sizeof(float), hipMemcpyDeviceToDevice, s));
+  return CRF_OK;
+}
+
+crf_status run_window(crf_context *ctx, const void *hb, const crf_layer_weights *W, const crf_lora_layer *lora,
+                      int l0, int h, const crf_kv_cache *kv, void *hout, hipStream_t s) {
+  if (h == 0 || kv->n_tokens == 0) return CRF_OK;
+  if (ctx->dims.dtype == CRF_BF16) return run_layers_bf16(ctx, hb, W, lora, l0, h, kv, hout, s);
+  return run_layers_f32(ctx, hb, W, lora, l0, h, kv, hout, s);
+}
+
+template <typename T>
+crf_status dmalloc(crf_context *ctx, T **p, size_t bytes) {
+  void *q = nullptr;
+  if (bytes == 0) bytes = 16;
+  hipError_t e = hipMalloc(&q, bytes);
+  if (e != hipSuccess) return fail(ctx, CRF_ERR_HIP, "hipMalloc(%zu): %s", bytes, hipGetErrorString(e));
+  *p = (T *)q;
+  return CRF_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *crf_status_string(crf_status s) {
+  switch (s) {
+    case CRF_OK: return "CRF_OK";
+    case CRF_ERR_INVALID_ARG: return "CRF_ERR_INVALID_ARG";
+    case CRF_ERR_SHAPE: return "CRF_ERR_SHAPE";
+    case CRF_ERR_RANGE: return "CRF_ERR_RANGE";
+    case CRF_ERR_UNSUPPORTED: return "CRF_ERR_UNSUPPORTED";
+    case CRF_ERR_WORKSPACE: return "CRF_ERR_WORKSPACE";
+    case CRF_ERR_HIP: return "CRF_ERR_HIP";
+    case CRF_ERR_DEVICE: return "CRF_ERR_DEVICE";
+  }
+  return "CRF_ERR_UNKNOWN";
+}
+
+int32_t crf_abi_version(void) { return CRF_ABI_VERSION; }
+
+const char *crf_last_error(const crf_context *ctx) { return ctx ? ctx->last_error.c_str() : g_last_error.c_str(); }
+
+crf_status crf_validate_dims(const crf_model_dims *dims) { return check_dims(nullptr, dims); }
+
+crf_status crf_validate_window(const crf_model_dims *dims, int32_t l0, int32_t h, const crf_kv_cache *kv) {
+  return check_window(nullptr, dims, l0, h, kv);
+}
+
+void crf_context_destroy(crf_context *ctx) {
+  if (!ctx) return;
+  void *bufs[] = {ctx->hres, ctx->xn, ctx->q, ctx->attn, ctx->act, ctx->u, ctx->proj, ctx->gu, ctx->rope_cs,
+                  ctx->d_err, ctx->drift_dev};
+  for (void *b : bufs)
+    if (b) (void)hipFree(b);
+  if (ctx->drift_host) (void)hipHostFree(ctx->drift_host);
+  if (ctx->drift_ev) (void)hipEventDestroy(ctx->drift_ev);
+  for (hipEvent_t e : ctx->timer.ev) (void)hipEventDestroy(e);
+  delete ctx;
+}
+
+crf_status crf_context_create(const crf_model_dims *dims, int32_t max_tokens, int32_t max_lora_rank,
+                              crf_context **out) {
+  if (!out) return fail(nullptr, CRF_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  crf_status st = check_dims(nullptr, dims);
+  if (st != CRF_OK) return st;
+  if (max_tokens < 1) return fail(nullptr, CRF_ERR_SHAPE, "max_tokens must be >= 1");
+  if (max_lora_rank < 0 || max_lora_rank > 64) return fail(nullptr, CRF_ERR_UNSUPPORTED, "max_lora_rank must be in [0, 64]");
+  crf_context *ctx = new crf_context();
+  ctx->dims = *dims;
+  ctx->max_tokens = max_tokens;
+  ctx->max_rank = max_lora_rank;
+  ctx->rank_pad = ((max_lora_rank + 15) / 16) * 16;
+  ctx->esz = dims->dtype == CRF_BF16 ? 2 : 4;
+  (void)hipGetDevice(&ctx->device);
+  const size_t T = (size_t)max_tokens, D = dims->d_model, dq = dq_of(*dims), dkv = dkv_of(*dims), f = dims->d_ffn;
+  const size_t e = ctx->esz;
+  auto cleanup = [&](crf_status s) {
+    if (s != CRF_OK) {
+      g_last_error = ctx->last_error;
+      crf_context_destroy(ctx);
+    }
+    return s;
+  };
+  if ((st = dmalloc(ctx, &ctx->hres, T * D * 4)) != CRF_OK) return cleanup(st);
+  if ((st = dmalloc(ctx, &ctx->xn, T * D * e)) != CRF_OK) return cleanup(st);
+  if ((st = dmalloc(ctx, &ctx->q, T * dq * e)) != CRF_OK) return cleanup(st);
+  if ((st = dmalloc(ctx, &ctx->attn, T * dq * e)) != CRF_OK) return cleanup(st);
+  if ((st = dmalloc(ctx, &ctx->act, T * f * e)) != CRF_OK) return cleanup(st);
+  if (dims->dtype == CRF_BF16) {
+    if ((st = dmalloc(ctx, &ctx->u, T * 3 * ctx->rank_pad * 2)) != CRF_OK) return cleanup(st);
+  } else {
+    if ((st = dmalloc(ctx, &ctx->u, T * (size_t)(max_lora_rank > 0 ? max_lora_rank : 1) * 4)) != CRF_OK)
+      return cleanup(st);
+    if ((st = dmalloc(ctx, &ctx->proj, T * (dq + 2 * dkv) * 4)) != CRF_OK) return cleanup(st);
+    if ((st = dmalloc(ctx, &ctx->gu, T * 2 * f * 4)) != CRF_OK) return cleanup(st);
+  }
+  if ((st = dmalloc(ctx, &ctx->rope_cs, T * (dims->head_dim / 2) * sizeof(float2))) != CRF_OK) return cleanup(st);
+  if ((st = dmalloc(ctx, &ctx->d_err, sizeof(int))) != CRF_OK) return cleanup(st);
+  hipError_t he = hipMemset(ctx->d_err, 0, sizeof(int));
+  if (he == hipSuccess) he = launch_rope_table(nullptr, ctx->rope_cs, max_tokens, dims->head_dim, dims->rope_theta);
+  if (he == hipSuccess) he = hipDeviceSynchronize();
+  if (he != hipSuccess) return cleanup(fail(ctx, CRF_ERR_HIP, "context init: %s", hipGetErrorString(he)));
+  *out = ctx;
+  return CRF_OK;
+}
+
+crf_status crf_recompute_window(crf_context *ctx, const crf_model_dims *dims, const void *hidden_at_boundary,
+                                const crf_layer_weights *base_weights, const crf_lora_layer *lora, int32_t l0,
+                                int32_t h, const crf_kv_cache *kv_cache, void *hidden_out, void *stream) {
+  if (!ctx) return fail(nullptr, CRF_ERR_INVALID_ARG, "context is NULL");
+  crf_status st = check_request(ctx, dims, hidden_at_boundary, base_weights, lora, l0, h, kv_cache, hidden_out,
+                                "crf_recompute_window");
+  if (st != CRF_OK) return st;
+  return run_window(ctx, hidden_at_boundary, base_weights, lora, l0, h, kv_cache, hidden_out, (hipStream_t)stream);
+}
+
+crf_status crf_recompute_window_batched(crf_context *ctx, const crf_model_dims *dims,
+                                        const crf_layer_weights *base_weights, int32_t n_items,
+                                        const crf_window_item *items, void *stream) {
+  if (!ctx) return fail(nullptr, CRF_ERR_INVALID_ARG, "context is NULL");
+  if (n_items < 0 || (n_items > 0 && !items)) return fail(ctx, CRF_ERR_INVALID_ARG, "items NULL or n_items < 0");
+  for (int i = 0; i < n_items; ++i) {
+    char what[64];
+    snprintf(what, sizeof what, "item %d", i);
+    const crf_window_item &it = items[i];
+    crf_status st = check_request(ctx, dims, it.hidden_at_boundary, base_weights, it.lora, it.l0, it.h, &it.kv,
+                                  it.hidden_out, what);
+    if (st != CRF_OK) return st;
+  }
+  for (int i = 0; i < n_items; ++i) {
+    const crf_window_item &it = items[i];
+    crf_status st = run_window(ctx, it.hidden_at_boundary, base_weights, it.lora, it.l0, it.h, &it.kv, it.hidden_out,
+                               (hipStream_t)stream);
+    if (st != CRF_OK) return st;
+  }
+  return CRF_OK;
+}
+
+crf_status crf_layer_drift(crf_context *ctx, const crf_model_dims *dims, const crf_lora_layer *current,
+                           int32_t n_versions, const crf_lora_layer *const *versions,
+                           const int32_t *anchor_version, const float *sensitivity, int32_t per_layer_only,
+                           float *drift_out, float *risk_out, float *sq_partial_out, void *stream) {
+  if (!ctx) return fail(nullptr, CRF_ERR_INVALID_ARG, "context is NULL");
+  crf_status st = check_dims(ctx, dims);
+  if (st != CRF_OK) return st;
+  if (!same_dims(*dims, ctx->dims)) return fail(ctx, CRF_ERR_INVALID_ARG, "dims differ from the context's");
+  if (!current || !versions || !anchor_version || !drift_out || !risk_out || n_versions < 1)
+    return fail(ctx, CRF_ERR_INVALID_ARG, "NULL argument or n_versions < 1");
+  const int L = dims->n_layers;
+  for (int l = 0; l < L; ++l)
+    if (anchor_version[l] < 0 || anchor_version[l] >= n_versions)
+      return fail(ctx, CRF_ERR_INVALID_ARG, "anchor_version[%d] = %d outside [0, %d)", l, anchor_version[l],
+                  n_versions);
+  const int64_t CH = 1 << 16;
+  std::vector<DriftSeg> segs;
+  std::vector<DriftChunk> chunks;
+  std::vector<int> first(n_versions * L), count(n_versions * L);
+  for (int v = 0; v < n_versions; ++v) {
+    if (!versions[v]) return fail(ctx, CRF_ERR_INVALID_ARG, "versions[%d] is NULL", v);
+    for (int l = 0; l < L; ++l) {
+      const int o = v * L + l;
+      first[o] = (int)chunks.size();
+      const crf_lora_layer &c = current[l], &vv = versions[v][l];
+      for (int t = 0; t < CRF_NUM_TARGETS && c.rank > 0; ++t) {
+        if (!c.A[t]) continue;
+        if (!c.B[t] || !vv.A[t] || !vv.B[t] || vv.rank != c.rank)
+          return fail(ctx, CRF_ERR_INVALID_ARG, "layer %d target %d missing or rank differs in version %d", l, t, v);
+        int d_out, d_in;
+        target_shape(*dims, t, d_out, d_in);
+        const int64_t na = (int64_t)c.rank * d_in, nb = (int64_t)d_out * c.rank;
+        const void *pa[2] = {c.A[t], c.B[t]}, *pb[2] = {vv.A[t], vv.B[t]};
+        const int64_t cnt[2] = {na, nb};
+        for (int k = 0; k < 2; ++k) {
+          const int si = (int)segs.size();
+          segs.push_back(DriftSeg{pa[k], pb[k], cnt[k], o});
+          for (int64_t s0 = 0; s0 < cnt[k]; s0 += CH) chunks.push_back(DriftChunk{si, s0, std::min(CH, cnt[k] - s0)});
+        }
+      }
+      count[o] = (int)chunks.size() - first[o];
+    }
+  }
+  // staging layout: segs | chunks | first | count | anchor | partials(double) | scratch(double)
+  auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
+  const size_t o_segs = 0, o_chunks = al(o_segs + segs.size() * sizeof(DriftSeg));
+  const size_t o_first = al(o_chunks + chunks.size() * sizeof(DriftChunk));
+  const size_t o_count = al(o_first + first.size() * sizeof(int));
+  const size_t o_anchor = al(o_count + count.size() * sizeof(int));
+  const size_t host_bytes = al(o_anchor + L * sizeof(int));
+  const size_t o_part = host_bytes, o_scr = al(o_part + (chunks.size() + 1) * sizeof(double));
+  const size_t dev_bytes = al(o_scr + first.size() * sizeof(double));
+  hipStream_t s = (hipStream_t)stream;
+  if (!ctx->drift_ev) HIP_TRY(ctx, hipEventCreateWithFlags(&ctx->drift_ev, hipEventDisableTiming));
+  if (ctx->drift_ev_recorded) HIP_TRY(ctx, hipEventSynchronize(ctx->drift_ev));
+  if (host_bytes > ctx->drift_host_bytes) {
+    if (ctx->drift_host) HIP_TRY(ctx, hipHostFree(ctx->drift_host));
+    ctx->drift_host = nullptr;
+    ctx->drift_host_bytes = 0;
+    HIP_TRY(ctx, hipHostMalloc(&ctx->drift_host, host_bytes, hipHostMallocDefault));
+    ctx->drift_host_bytes = host_bytes;
+  }
+  if (dev_bytes > ctx->drift_dev_bytes) {
+    HIP_TRY(ctx, hipStreamSynchronize(s));
+    if (ctx->drift_dev) HIP_TRY(ctx, hipFree(ctx->drift_dev));
+    ctx->drift_dev = nullptr;
+    ctx->drift_dev_bytes = 0;
+    HIP_TRY(ctx, hipMalloc(&ctx->drift_dev, dev_bytes));
+    ctx->drift_dev_bytes = dev_bytes;
+  }
+  char *hb = (char *)ctx->drift_host, *db = (char *)ctx->drift_dev;
+  memcpy(hb + o_segs, segs.data(), segs.size() * sizeof(DriftSeg));
+  memcpy(hb + o_chunks, chunks.data(), chunks.size() * sizeof(DriftChunk));
+  memcpy(hb + o_first, first.data(), first.size() * sizeof(int));
+  memcpy(hb + o_count, count.data(), count.size() * sizeof(int));
+  memcpy(hb + o_anchor, anchor_version, L * sizeof(int));
+  HIP_TRY(ctx, hipMemcpyAsync(db, hb, host_bytes, hipMemcpyHostToDevice, s));
+  HIP_TRY(ctx, hipEventRecord(ctx->drift_ev, s));
+  ctx->drift_ev_recorded = true;
+  const bool f32 = dims->dtype == CRF_F32;
+  LAUNCH(ctx, s, CRF_KK_DRIFT,
+         launch_drift_partials(s, (const DriftSeg *)(db + o_segs), (const DriftChunk *)(db + o_chunks),
+                               (int)chunks.size(), f32, (double *)(db + o_part)));
+  LAUNCH(ctx, s, CRF_KK_DRIFT,
+         launch_drift_finalize(s, (const double *)(db + o_part), (const int *)(db + o_first),
+                               (const int *)(db + o_count), n_versions, L, (const int *)(db + o_anchor), sensitivity,
+                               per_layer_only, drift_out, risk_out, sq_partial_out, (double *)(db + o_scr)));
+  return CRF_OK;
+}
+
+crf_status crf_context_device_errors(crf_context *ctx, int32_t *flags_out) {
+  if (!ctx || !flags_out) return fail(ctx, CRF_ERR_INVALID_ARG, "NULL argument");
+  HIP_TRY(ctx, hipDeviceSynchronize());
+  int v = 0;
+  HIP_TRY(ctx, hipMemcpy(&v, ctx->d_err, sizeof(int), hipMemcpyDeviceToHost));
+  HIP_TRY(ctx, hipMemset(ctx->d_err, 0, sizeof(int)));
+  *flags_out = v;
+  return CRF_OK;
+}
+
+crf_status crf_context_set_timing(crf_context *ctx, int32_t enable) {
+  if (!ctx) return fail(nullptr, CRF_ERR_INVALID_ARG, "context is NULL");
+  ctx->timer.on = enable != 0;
+  return CRF_OK;
+}
+
+crf_status crf_context_read_timing(crf_context *ctx, float *ms_out, int32_t *count_out, int32_t n_kinds) {
+  if (!ctx || !ms_out || !count_out || n_kinds < 0) return fail(ctx, CRF_ERR_INVALID_ARG, "bad argument");
+  for (int k = 0; k < n_kinds; ++k) {
+    ms_out[k] = 0.f;
+    count_out[k] = 0;
+  }
+  Timer &t = ctx->timer;
+  if (t.used > 0) HIP_TRY(ctx, hipEventSynchronize(t.ev[2 * t.used - 1]));
+  for (size_t i = 0; i < t.used; ++i) {
+    float ms = 0.f;
+    HIP_TRY(ctx, hipEventElapsedTime(&ms, t.ev[2 * i], t.ev[2 * i + 1]));
+    const int k = t.kind[i];
+    if (k >= 0 && k < n_kinds) {
+      ms_out[k] += ms;
+      count_out[k] += 1;
+    }
+  }
+  t.used = 0;
+  return CRF_OK;
+}
+
+}  // extern "C"

