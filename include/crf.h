@@ -146,8 +146,9 @@ crf_status crf_validate_dims(const crf_model_dims *dims);
  * l0 + h <= n_layers (else RANGE), and the cache geometry: page_size >= 1,
  * n_tokens >= 0, n_tokens <= n_pages * page_size, page_stride >=
  * n_kv_heads*page_size*head_dim, layer_stride >= n_pages*page_stride (else
- * SHAPE), non-null pools and block table when h > 0 and n_tokens > 0 (else
- * INVALID_ARG).  Touches no device. */
+ * SHAPE), one layer of a pool (n_pages*page_stride elements) under 2 GiB
+ * (else UNSUPPORTED), non-null pools and block table when h > 0 and
+ * n_tokens > 0 (else INVALID_ARG).  Touches no device. */
 crf_status crf_validate_window(const crf_model_dims *dims, int32_t l0, int32_t h, const crf_kv_cache *kv);
 
 /* Bounded recomputation R_{l0,h} (Sec. 4.2 "Executable restart"; supplementary

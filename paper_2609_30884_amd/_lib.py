@@ -12,7 +12,7 @@ import os
 from typing import Dict, Iterable, List, Mapping, Optional, Sequence, Tuple
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libcrf.so")
+LIB_PATH = os.environ.get("CRF_LIBRARY") or os.path.join(HERE, "libcrf.so")
 
 TARGETS = ("q", "k", "v", "o", "gate", "up", "down")
 NUM_TARGETS = 7

@@ -130,6 +130,8 @@ crf_status check_window(crf_context *ctx, const crf_model_dims *d, int32_t l0, i
     return fail(ctx, CRF_ERR_SHAPE, "page_stride %lld < n_kv_heads*page_size*head_dim", (long long)kv->page_stride);
   if (kv->layer_stride < (int64_t)kv->n_pages * kv->page_stride)
     return fail(ctx, CRF_ERR_SHAPE, "layer_stride %lld < n_pages*page_stride", (long long)kv->layer_stride);
+  if ((int64_t)kv->n_pages * kv->page_stride * (d->dtype == CRF_BF16 ? 2 : 4) >= ((int64_t)1 << 31))
+    return fail(ctx, CRF_ERR_UNSUPPORTED, "one layer of the KV pool must be smaller than 2 GiB");
   if (h > 0 && kv->n_tokens > 0 && (!kv->k_pool || !kv->v_pool || !kv->block_table))
     return fail(ctx, CRF_ERR_INVALID_ARG, "k_pool, v_pool and block_table must be non-NULL");
   return CRF_OK;

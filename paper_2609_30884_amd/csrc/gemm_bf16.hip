@@ -75,10 +75,17 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(const GemmParams p) {
 
   // ---- global -> register loader: 8 chunks of X and 8 of W per thread per slice.
   // Thread rows are lr + 32*i; W rows come in four 64-row groups (i = 2q, 2q+1),
-  // each contiguous inside one weight segment.
+  // each contiguous inside one weight segment.  Buffer loads: the per-lane byte
+  // offsets are fixed, the slice offset k0 goes in the scalar operand, and X rows
+  // past M fall outside the X resource and read as zero.
   const int lc = tid % 8, lr = tid / 8;  // chunk, first row
-  const bf16 *xsrc = p.X + (int64_t)(m0 + lr) * p.ldx + lc * 8;
-  const int64_t xstep = (int64_t)32 * p.ldx;
+  const __amdgpu_buffer_rsrc_t xres = make_rsrc(p.X, (uint32_t)((int64_t)p.M * p.ldx * 2));
+  uint32_t xoff[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int r = m0 + lr + 32 * i;
+    xoff[i] = r < p.M ? (uint32_t)(((int64_t)r * p.ldx + lc * 8) * 2) : CRF_OOB;
+  }
   const bf16 *wsrc[4];
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
@@ -90,9 +97,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(const GemmParams p) {
   auto gload = [&](int k0) {
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      u32x4 v = {0u, 0u, 0u, 0u};
-      if (m0 + lr + 32 * i < p.M) v = ld16(xsrc + i * xstep + k0);
-      px[i] = v;
+      px[i] = bld16(xres, xoff[i], (uint32_t)k0 * 2);
       pw[i] = ld16(wsrc[i / 2] + (i % 2) * wstep + k0);
     }
   };
@@ -297,6 +302,7 @@ hipError_t go(hipStream_t s, const GemmParams &p) {
 hipError_t launch_gemm_bf16(hipStream_t s, GemmEpi epi, int hd, const GemmParams &p) {
   if (p.M <= 0 || p.N <= 0) return hipSuccess;
   if (p.K % BK) return hipErrorInvalidValue;
+  if ((int64_t)p.M * p.ldx * 2 >= (int64_t)CRF_OOB) return hipErrorInvalidValue;  // X must fit one buffer resource
   switch (epi) {
     case EPI_RESID: return go<EPI_RESID, 128>(s, p);
     case EPI_SWIGLU: return go<EPI_SWIGLU, 128>(s, p);
