@@ -6,6 +6,11 @@ rank-16 LoRA on all seven projections, paged bf16 KV cache with 16-token
 pages), inputs resident in HBM before the timed region.  Prints one JSON line.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+
+Other workloads (one JSON line each): tiny_f32, qwen15b_4k, qwen7b_16k_suffix
+(the 24-layer affected suffix), qwen15b_mixed8 (8 ragged stale caches through
+the batched call) and drift (crf_layer_drift over 28 layers and 4 stored
+adapter versions at 1.5B shapes).
 """
 from __future__ import annotations
 
@@ -93,6 +98,10 @@ def main():
     crf.load()
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
+    if args.workload == "drift":
+        return bench_drift(args)
+    if args.workload == "qwen15b_mixed8":
+        return bench_mixed(args)
     wl = syn.WORKLOADS[args.workload]
     dims = wl.dims
     win = wl.window
@@ -191,6 +200,112 @@ def main():
             "sample": f"fp64 numpy oracle, first {ns} of {win.n_tokens} prefix tokens through layers "
                       f"[{win.l0},{win.l0 + win.h}) ({dt:.1f} s; causal attention over that shorter prefix)",
         }
+    print(json.dumps(out), flush=True)
+
+
+def _timed(step, steps, warmup, ctx=None):
+    import torch
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    if ctx is not None:
+        ctx.set_timing(True)
+        ctx.read_timing()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    timing = None
+    if ctx is not None:
+        ctx.set_timing(False)
+        timing = ctx.read_timing()
+    return elapsed, timing
+
+
+def bench_mixed(args):
+    """8 independent stale caches (1.5B shapes, ragged n, own l0/h/adapter) in one
+    crf_recompute_window_batched call per step."""
+    import torch
+    import paper_2609_30884_amd as crf
+    import synthetic as syn
+    from synthetic.device import build_case
+    wl = syn.WORKLOADS["qwen15b_mixed8"]
+    dims = wl.dims
+    layers = sorted({l for w in wl.windows for l in range(w.l0, w.l0 + w.h)})
+    # one base model (weights of every layer any item touches), one adapter version per item
+    cases = [build_case(wl, args.seed, window=w, item=i, layers=layers, keep_host=False, with_weights=(i == 0))
+             for i, w in enumerate(wl.windows)]
+    cd = crf.make_dims(dims.n_layers, dims.d_model, dims.n_q_heads, dims.n_kv_heads, dims.head_dim, dims.d_ffn,
+                       dims.rms_eps, dims.rope_theta, dims.dtype)
+    ctx = crf.Context(cd, max(w.n_tokens for w in wl.windows), wl.lora_rank)
+    weights = crf.layer_weights_array(cases[0].weights_dev)
+    keep, items = [], []
+    for c in cases:
+        la = crf.lora_array(c.lora_dev, dims.n_layers)
+        keep.append(la)
+        kv = crf.kv_cache(c.k_pool, c.v_pool, c.block_table_dev, c.window.n_tokens, wl.page_size)
+        items.append(crf.window_item(c.hidden_dev, la, c.window.l0, c.window.h, kv, c.hidden_out))
+    stream = torch.cuda.current_stream()
+    elapsed, timing = _timed(lambda: crf.recompute_window_batched(ctx, cd, weights, items, stream), args.steps,
+                             args.warmup, ctx)
+    tl = sum(w.n_tokens * w.h for w in wl.windows)
+    f = sum(window_flops(dims, w.n_tokens, w.h, wl.lora_rank, wl.lora_targets)[0] for w in wl.windows)
+    ms = 1e3 * elapsed / args.steps
+    out = {
+        "metric": METRIC, "value": round(tl * args.steps / elapsed, 1), "unit": "token-layers/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 3), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "qwen15b_mixed8: 8 stale caches, Qwen2.5-1.5B shapes, ragged n/l0/h, own LoRA "
+                               "version each, one batched call",
+                   "items": [[w.n_tokens, w.l0, w.h] for w in wl.windows]},
+        "mfma_util": round(f / (elapsed / args.steps) / PEAK_BF16, 4),
+        "kernels": {k: {"avg_ms": round(v[0] / v[1], 4), "launches": v[1]} for k, v in timing.items() if v[1]},
+    }
+    print(json.dumps(out), flush=True)
+
+
+def bench_drift(args):
+    """crf_layer_drift over 28 layers x 4 stored versions (1.5B shapes, rank 16 on q,k,v,o)."""
+    import numpy as np
+    import torch
+    import paper_2609_30884_amd as crf
+    import synthetic as syn
+    from synthetic.device import lora_to_dev
+    wl = syn.WORKLOADS["qwen15b_mixed8"]
+    dims = wl.dims
+    n_versions = 4
+    states = [[lora_to_dev(syn.gen_lora_layer(wl, args.seed, l, v), wl.lora_rank, 1.0, dims)
+               for l in range(dims.n_layers)] for v in range(n_versions + 1)]
+    cd = crf.make_dims(dims.n_layers, dims.d_model, dims.n_q_heads, dims.n_kv_heads, dims.head_dim, dims.d_ffn,
+                       dims.rms_eps, dims.rope_theta, dims.dtype)
+    ctx = crf.Context(cd, 1, wl.lora_rank)
+    cur = crf.lora_array(states[-1], dims.n_layers)
+    vers = [crf.lora_array(s_, dims.n_layers) for s_ in states[:-1]]
+    anchors = syn.gen_anchor_versions(dims.n_layers, n_versions, args.seed)
+    sens = torch.from_numpy(syn.gen_sensitivity(dims.n_layers, args.seed)).cuda()
+    drift = torch.empty(dims.n_layers, device="cuda")
+    risk = torch.empty_like(drift)
+    stream = torch.cuda.current_stream()
+    elapsed, timing = _timed(lambda: crf.layer_drift(ctx, cd, cur, vers, anchors, sens, drift, risk, None,
+                                                      stream=stream), args.steps, args.warmup, ctx)
+    n_params = sum(int(a.numel() + b.numel()) for l in states[-1] for a, b in l["targets"].values())
+    bytes_per_call = 2 * n_params * 2 * n_versions   # current + version, bf16, per version
+    ms = 1e3 * elapsed / args.steps
+    kern_ms = timing["drift"][0] / max(timing["drift"][1], 1) * 1e-3 * 2  # two kernels per call
+    out = {
+        "metric": "adapter drift scoring: ms per call over all layers and stored versions", "value": round(ms, 4),
+        "unit": "ms", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "higher_is_better": False, "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"drift: {dims.n_layers} layers, {n_versions} stored versions, {n_params} adapter "
+                               f"parameters per version"},
+        "roofline": {"bound": "hbm", "achieved": round(bytes_per_call / (timing['drift'][0] / args.steps * 1e-3) / 1e9, 1),
+                     "peak": PEAK_HBM / 1e9, "unit": "GB/s",
+                     "frac": round(bytes_per_call / (timing['drift'][0] / args.steps * 1e-3) / PEAK_HBM, 4),
+                     "traffic": None},
+        "kernels": {k: {"avg_ms": round(v[0] / v[1], 4), "launches": v[1]} for k, v in timing.items() if v[1]},
+    }
     print(json.dumps(out), flush=True)
 
 

@@ -37,22 +37,22 @@ def hipcc() -> str:
     return p
 
 
-def _compile(src: str, obj_dir: str = OBJ, extra=()) -> str:
+def _compile(src: str, obj_dir: str = OBJ, extra=(), csrc: str = CSRC) -> str:
     out = os.path.join(obj_dir, os.path.splitext(src)[0] + ".o")
-    cmd = [hipcc(), "-x", "hip", "-c", os.path.join(CSRC, src), "-o", out] + CFLAGS + list(extra)
+    cmd = [hipcc(), "-x", "hip", "-c", os.path.join(csrc, src), "-o", out] + CFLAGS + list(extra)
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"compile {src} failed:\n{' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
     return out
 
 
-def build(verbose: bool = True, lib: str = LIB, obj_dir: str = OBJ, defines=()) -> str:
-    """Compile and link.  `defines` (e.g. ["-DCRF_ATTN_QPW=1"]) select tuning
-    variants for a library written to `lib`."""
+def build(verbose: bool = True, lib: str = LIB, obj_dir: str = OBJ, defines=(), csrc: str = CSRC) -> str:
+    """Compile and link.  `lib`, `obj_dir`, `defines` and `csrc` let a tuning
+    variant be built next to the default library."""
     os.makedirs(obj_dir, exist_ok=True)
     jobs = min(len(SOURCES), max(1, min(8, os.cpu_count() or 1)))
     with cf.ThreadPoolExecutor(jobs) as ex:
-        objs = list(ex.map(lambda s: _compile(s, obj_dir, defines), SOURCES))
+        objs = list(ex.map(lambda s: _compile(s, obj_dir, defines, csrc), SOURCES))
     tmp = lib + ".tmp"
     cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp] + objs
     r = subprocess.run(cmd, capture_output=True, text=True)

@@ -9,8 +9,13 @@
 //
 // Tiling for CDNA4: 256x256 output tile per 256-thread workgroup, 2x2 waves of
 // 128x128, v_mfma_f32_32x32x16_bf16, K staged through LDS in 64-wide slices,
-// double-buffered (2 x 64 KB), with the next slice prefetched into registers
-// while the current one is consumed.  The weight operand takes the MFMA "A"
+// double-buffered (2 x 64 KB).  Slices move global -> LDS by DMA
+// (buffer_load ... lds): no staging registers and no LDS stores in the waves'
+// instruction stream; the next slice's DMA is issued right after the single
+// per-slice barrier and overlaps the current slice's MFMAs, and within a slice
+// the LDS fragment reads of step s+1 are issued ahead of step s's MFMAs.  Rows
+// past M (or past N) get an out-of-range offset and arrive as zeros.  The
+// weight operand takes the MFMA "A"
 // role so each lane ends up holding 4 consecutive output features of one
 // token, which makes every epilogue lane-local (a rotary pair (f, f+hd/2) and a
 // gate/up pair live in the same lane).  16-byte LDS chunks are XOR-swizzled by
@@ -20,11 +25,15 @@
 namespace crf {
 namespace {
 
-constexpr int BM = 256, BN = 256, BK = 64;
+constexpr int BM = 256, BN = 256, BK = 32;
+constexpr int STAGES = 4;  // LDS ring depth: slice kt+3 is in flight while slice kt is consumed
 constexpr int NT = 256;
 constexpr int GROUP_M = 8;
 
-CRF_DEV int swz(int row, int chunk) { return row * BK + ((chunk ^ ((row >> 1) & 7)) << 3); }
+// 64-byte rows (32 bf16), four 16-byte chunks; chunk c of row r sits at
+// position c ^ ((r / 4) % 4), so the 16 rows a ds_read_b128 quarter-wave
+// touches hit 16 distinct 4-bank groups.
+CRF_DEV int swz(int row, int chunk) { return row * BK + ((chunk ^ ((row >> 2) & 3)) << 3); }
 
 template <int EPI>
 CRF_DEV const bf16 *weight_row(const GemmParams &p, int r) {
@@ -56,8 +65,8 @@ CRF_DEV int segment_of(const GemmParams &p, int r, int &local) {
 template <int EPI, int HD>
 __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(const GemmParams p) {
   extern __shared__ __align__(16) bf16 smem[];
-  bf16 *const lds_x = smem;                  // [2][BM*BK]
-  bf16 *const lds_w = smem + 2 * BM * BK;    // [2][BN*BK]
+  bf16 *const lds_x = smem;                       // [STAGES][BM*BK]
+  bf16 *const lds_w = smem + STAGES * BM * BK;    // [STAGES][BN*BK]
 
   const int tiles_m = (p.M + BM - 1) / BM;
   const int tiles_n = (p.N + BN - 1) / BN;
@@ -69,46 +78,46 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(const GemmParams p) {
   const int tn = (t % group) / gm;
   const int m0 = tm * BM, n0 = tn * BN;
 
-  const int tid = threadIdx.x, lane = tid % 64, wave = tid / 64;
+  const int tid = threadIdx.x, lane = tid % 64;
+  const int wave = __builtin_amdgcn_readfirstlane(tid / 64);  // uniform: keeps DMA targets scalar
   const int wm = wave & 1, wn = wave >> 1;
   const int g = lane / 32, l32 = lane % 32;
 
-  // ---- global -> register loader: 8 chunks of X and 8 of W per thread per slice.
-  // Thread rows are lr + 32*i; W rows come in four 64-row groups (i = 2q, 2q+1),
-  // each contiguous inside one weight segment.  Buffer loads: the per-lane byte
-  // offsets are fixed, the slice offset k0 goes in the scalar operand, and X rows
-  // past M fall outside the X resource and read as zero.
-  const int lc = tid % 8, lr = tid / 8;  // chunk, first row
+  // ---- global -> LDS DMA.  A slice of one operand is 256 rows x 32 k = 16 x 1 KB
+  // blocks; wave w moves blocks 4j + w (j = 0..3).  Inside a block, lane L writes
+  // LDS bytes [16 L, 16 L + 16): row 16*block + L/4, swizzled position L%4, which
+  // holds logical k-chunk (L%4) ^ ((row/4)%4) of that row.
+  typedef __attribute__((address_space(3))) void lds_t;
+  typedef __attribute__((address_space(3))) char lds_c;
   const __amdgpu_buffer_rsrc_t xres = make_rsrc(p.X, (uint32_t)((int64_t)p.M * p.ldx * 2));
-  uint32_t xoff[8];
+  uint32_t xoff[4], woff[4];
+  __amdgpu_buffer_rsrc_t wres[4];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int r = m0 + lr + 32 * i;
-    xoff[i] = r < p.M ? (uint32_t)(((int64_t)r * p.ldx + lc * 8) * 2) : CRF_OOB;
+  for (int j = 0; j < 4; ++j) {
+    const int blk = 4 * j + wave;
+    const int row = blk * 16 + lane / 4;
+    const int c = (lane % 4) ^ ((row >> 2) & 3);
+    const int xr = m0 + row;
+    xoff[j] = xr < p.M ? (uint32_t)(((int64_t)xr * p.ldx + c * 8) * 2) : CRF_OOB;
+    // weight rows: the 16 rows of a block sit in one 64-row group, inside one segment
+    const int wr = n0 + row;
+    int lr0, local;
+    const int sg = segment_of<EPI>(p, min(n0 + blk * 16, p.N - 1), lr0);
+    const int seg_rows = EPI == EPI_QKV ? (sg == 0 ? p.seg1 : sg == 1 ? p.seg2 - p.seg1 : p.N - p.seg2)
+                                        : (EPI == EPI_SWIGLU ? p.N / 2 : p.N);
+    segment_of<EPI>(p, min(wr, p.N - 1), local);
+    wres[j] = make_rsrc(p.w[sg], (uint32_t)((int64_t)seg_rows * p.K * 2));
+    woff[j] = wr < p.N ? (uint32_t)(((int64_t)local * p.K + c * 8) * 2) : CRF_OOB;
   }
-  const bf16 *wsrc[4];
+  auto dma = [&](int k0, int stage) {
+    lds_c *dx = (lds_c *)(lds_x + stage * BM * BK);
+    lds_c *dw = (lds_c *)(lds_w + stage * BN * BK);
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int r = n0 + 64 * q + lr;
-    wsrc[q] = (r < p.N ? weight_row<EPI>(p, r) : p.w[0]) + lc * 8;
-  }
-  const int64_t wstep = (int64_t)32 * p.K;
-  u32x4 px[8], pw[8];
-  auto gload = [&](int k0) {
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      px[i] = bld16(xres, xoff[i], (uint32_t)k0 * 2);
-      pw[i] = ld16(wsrc[i / 2] + (i % 2) * wstep + k0);
-    }
-  };
-  auto lstore = [&](int buf) {
-    bf16 *dx = lds_x + buf * BM * BK;
-    bf16 *dw = lds_w + buf * BN * BK;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int r = lr + 32 * i;
-      st16(dx + swz(r, lc), px[i]);
-      st16(dw + swz(r, lc), pw[i]);
+    for (int j = 0; j < 4; ++j) {
+      const int blk = 4 * j + wave;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(xres, (lds_t *)(dx + blk * 1024), 16, xoff[j], (uint32_t)k0 * 2, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(wres[j], (lds_t *)(dw + blk * 1024), 16, woff[j], (uint32_t)k0 * 2, 0,
+                                               0);
     }
   };
 
@@ -151,32 +160,60 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(const GemmParams p) {
     }
   }
 
-  const int nk = p.K / BK;
-  gload(0);
-  lstore(0);
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) gload((kt + 1) * BK);
-    const bf16 *sx = lds_x + buf * BM * BK;
-    const bf16 *sw = lds_w + buf * BN * BK;
+  const int nk = p.K / BK;  // >= 2 (K is a multiple of 64)
+  auto frag = [&](int stage, int s, bf16x8 (&fa)[4], bf16x8 (&fb)[4]) {
+    const bf16 *sx = lds_x + stage * BM * BK;
+    const bf16 *sw = lds_w + stage * BN * BK;
 #pragma unroll
-    for (int s = 0; s < BK / 16; ++s) {
-      bf16x8 a[4], b[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int rw = wn * 128 + 32 * i + l32;
-        a[i] = as_bf16x8(ld16(sw + swz(rw, 2 * s + g)));
-        const int rx = wm * 128 + 32 * i + l32;
-        b[i] = as_bf16x8(ld16(sx + swz(rx, 2 * s + g)));
-      }
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = mfma32(a[i], b[j], acc[i][j]);
+    for (int i = 0; i < 4; ++i) {
+      fa[i] = as_bf16x8(ld16(sw + swz(wn * 128 + 32 * i + l32, 2 * s + g)));
+      fb[i] = as_bf16x8(ld16(sx + swz(wm * 128 + 32 * i + l32, 2 * s + g)));
     }
-    if (kt + 1 < nk) lstore(buf ^ 1);
-    __syncthreads();
+  };
+  // Wait for this wave's DMA of slice `kt` (later slices may stay in flight:
+  // 8 DMA instructions per slice), then a bare barrier publishes every wave's
+  // part.  Reads of earlier slices are complete (lgkmcnt(0)) before it, so a
+  // DMA issued after it may reuse their stage.
+  auto slice_ready = [&](int kt) {
+    const int later = min(nk - 1 - kt, STAGES - 2);
+    if (later >= 2)
+      asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
+    else if (later == 1)
+      asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+    else
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  };
+  // prologue: three slices in flight, slice 0 published, its step-0 fragments loaded
+#pragma unroll
+  for (int st = 0; st < STAGES - 1; ++st)
+    if (st < nk) dma(st * BK, st);
+  slice_ready(0);
+  bf16x8 a0[4], b0[4], a1[4], b1[4];
+  frag(0, 0, a0, b0);
+  // Steady state per slice kt: [step-1 reads of kt, DMA of kt+3] -> step-0 MFMAs ->
+  // publish slice kt+1 -> [step-0 reads of kt+1] -> step-1 MFMAs.  Fragments are
+  // always read one MFMA group ahead, and the barrier sits between the groups.
+  for (int kt = 0; kt < nk; ++kt) {
+    const int stage = kt % STAGES;
+    frag(stage, 1, a1, b1);
+    if (kt + STAGES - 1 < nk) dma((kt + STAGES - 1) * BK, (kt + STAGES - 1) % STAGES);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[i][j] = mfma32(a0[i], b0[j], acc[i][j]);
+    __builtin_amdgcn_sched_barrier(0);
+    if (kt + 1 < nk) {
+      slice_ready(kt + 1);
+      frag((kt + 1) % STAGES, 0, a0, b0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[i][j] = mfma32(a1[i], b1[j], acc[i][j]);
+    __builtin_amdgcn_sched_barrier(0);
   }
 
   // ---- epilogues
@@ -285,7 +322,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(const GemmParams p) {
 template <int EPI, int HD>
 hipError_t go(hipStream_t s, const GemmParams &p) {
   const int tiles = ((p.M + BM - 1) / BM) * ((p.N + BN - 1) / BN);
-  const size_t lds = (size_t)2 * (BM + BN) * BK * sizeof(bf16);
+  const size_t lds = (size_t)STAGES * (BM + BN) * BK * sizeof(bf16);
   static bool attr_set = false;
   if (!attr_set) {
     hipError_t e = hipFuncSetAttribute((const void *)gemm_bf16_kernel<EPI, HD>,

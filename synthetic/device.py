@@ -60,7 +60,8 @@ def lora_to_dev(lora: Dict[str, Tuple[np.ndarray, np.ndarray]], rank: int, scale
 
 def build_case(wl: Workload, seed: int, window: Optional[Window] = None, lora_version: int = 1,
                layers: Optional[Sequence[int]] = None, with_bias: bool = False, keep_host: bool = True,
-               item: int = 0, device="cuda", hidden: Optional[np.ndarray] = None) -> DeviceCase:
+               item: int = 0, device="cuda", hidden: Optional[np.ndarray] = None,
+               with_weights: bool = True) -> DeviceCase:
     """Generate and upload everything one window needs.
 
     layers: which layers get weights (default: the window's); the K/V pools
@@ -74,14 +75,16 @@ def build_case(wl: Workload, seed: int, window: Optional[Window] = None, lora_ve
     c.weights_dev = [None] * dims.n_layers
     c.lora_dev = [None] * dims.n_layers
     for l in layers:
-        w = gen_layer_weights(wl, seed, l, with_bias=with_bias)
         lo = gen_lora_layer(wl, seed, l, lora_version, item=item)
-        c.weights_dev[l] = {k: to_dev(v, dims, device) for k, v in w.items()}
         c.lora_dev[l] = lora_to_dev(lo, wl.lora_rank, wl.lora_scale, dims)
         if keep_host:
-            c.weights[l] = w
             c.lora[l] = lo
-        del w
+        if with_weights:
+            w = gen_layer_weights(wl, seed, l, with_bias=with_bias)
+            c.weights_dev[l] = {k: to_dev(v, dims, device) for k, v in w.items()}
+            if keep_host:
+                c.weights[l] = w
+            del w
     h = gen_hidden(wl, seed, win.n_tokens, item) if hidden is None else hidden
     c.hidden_dev = to_dev(h, dims, device)
     c.hidden_out = torch.empty_like(c.hidden_dev)
