@@ -55,6 +55,13 @@ CRF_DEV u32x4 bld16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
 }
 constexpr uint32_t CRF_OOB = 0x80000000u;  // any offset >= this is outside every resource we build
 
+// 16-byte-per-lane DMA from a buffer resource straight into LDS: lane L's bytes
+// land at lds + 16 L (lds must be wave-uniform).
+typedef __attribute__((address_space(3))) char lds_char;
+CRF_DEV void dma16(__amdgpu_buffer_rsrc_t r, lds_char *lds, uint32_t voff, uint32_t soff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void *)lds, 16, voff, soff, 0, 0);
+}
+
 CRF_DEV float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);

@@ -7,15 +7,16 @@
 //   EPI_RESID  fp32 residual update (attention output / down projection);
 //   EPI_SWIGLU silu(gate) * up with gate and up rows interleaved per 64 features.
 //
-// Tiling for CDNA4: 256x256 output tile per 256-thread workgroup, 2x2 waves of
-// 128x128, v_mfma_f32_32x32x16_bf16, K staged through LDS in 64-wide slices,
-// double-buffered (2 x 64 KB).  Slices move global -> LDS by DMA
-// (buffer_load ... lds): no staging registers and no LDS stores in the waves'
-// instruction stream; the next slice's DMA is issued right after the single
-// per-slice barrier and overlaps the current slice's MFMAs, and within a slice
-// the LDS fragment reads of step s+1 are issued ahead of step s's MFMAs.  Rows
-// past M (or past N) get an out-of-range offset and arrive as zeros.  The
-// weight operand takes the MFMA "A"
+// Tiling for CDNA4: a 256x256 output tile per workgroup, either 4 waves of
+// 128x128 (one wave per SIMD) or 8 waves of 128x64 (two waves per SIMD, so one
+// wave issues MFMAs while the other waits on LDS or memory); every wave owns
+// 128 output features.  v_mfma_f32_32x32x16_bf16; K staged through LDS in
+// 64-wide slices, double-buffered (2 x 64 KB).  Slices move global -> LDS by
+// DMA (buffer_load ... lds): no staging registers and no LDS stores in the
+// waves' instruction stream; slice kt+2's DMA is issued right after the single
+// per-slice barrier and overlaps slice kt+1's MFMAs, and fragment reads run one
+// MFMA group ahead.  Rows past M (or past N) get an out-of-range offset and
+// arrive as zeros.  The weight operand takes the MFMA "A"
 // role so each lane ends up holding 4 consecutive output features of one
 // token, which makes every epilogue lane-local (a rotary pair (f, f+hd/2) and a
 // gate/up pair live in the same lane).  16-byte LDS chunks are XOR-swizzled by
@@ -25,15 +26,14 @@
 namespace crf {
 namespace {
 
-constexpr int BM = 256, BN = 256, BK = 32;
-constexpr int STAGES = 4;  // LDS ring depth: slice kt+3 is in flight while slice kt is consumed
-constexpr int NT = 256;
+constexpr int BM = 256, BN = 256, BK = 64;
+constexpr int STAGES = 2;
 constexpr int GROUP_M = 8;
 
-// 64-byte rows (32 bf16), four 16-byte chunks; chunk c of row r sits at
-// position c ^ ((r / 4) % 4), so the 16 rows a ds_read_b128 quarter-wave
-// touches hit 16 distinct 4-bank groups.
-CRF_DEV int swz(int row, int chunk) { return row * BK + ((chunk ^ ((row >> 2) & 3)) << 3); }
+// 128-byte rows (64 bf16), eight 16-byte chunks; chunk c of row r sits at
+// position c ^ ((r / 2) % 8): the 16 rows a ds_read_b128 quarter-wave touches
+// hit 16 distinct 4-bank groups.
+CRF_DEV int swz(int row, int chunk) { return row * BK + ((chunk ^ ((row >> 1) & 7)) << 3); }
 
 template <int EPI>
 CRF_DEV const bf16 *weight_row(const GemmParams &p, int r) {
@@ -62,8 +62,16 @@ CRF_DEV int segment_of(const GemmParams &p, int r, int &local) {
   return (r >> 6) & 1;
 }
 
-template <int EPI, int HD>
-__global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(const GemmParams p) {
+// WAVES = 4: 2 (features) x 2 (tokens) waves of 128 x 128.
+// WAVES = 8: 2 (features) x 4 (tokens) waves of 128 x 64.
+template <int EPI, int HD, int WAVES>
+__global__ __launch_bounds__(64 * WAVES, 1) void gemm_bf16_kernel(const GemmParams p) {
+  constexpr int NT = 64 * WAVES;
+  constexpr int WM_COUNT = WAVES / 2;      // token groups
+  constexpr int WTM = BM / WM_COUNT;       // tokens per wave: 128 or 64
+  constexpr int NJ = WTM / 32;             // 32-token blocks per wave
+  constexpr int BLK = (BM / 8) / WAVES;    // 1 KB DMA blocks per operand per wave per slice
+  constexpr int DMA_PER_SLICE = 2 * BLK;
   extern __shared__ __align__(16) bf16 smem[];
   bf16 *const lds_x = smem;                       // [STAGES][BM*BK]
   bf16 *const lds_w = smem + STAGES * BM * BK;    // [STAGES][BN*BK]
@@ -80,29 +88,27 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(const GemmParams p) {
 
   const int tid = threadIdx.x, lane = tid % 64;
   const int wave = __builtin_amdgcn_readfirstlane(tid / 64);  // uniform: keeps DMA targets scalar
-  const int wm = wave & 1, wn = wave >> 1;
+  const int wn = wave / WM_COUNT, wm = wave % WM_COUNT;
   const int g = lane / 32, l32 = lane % 32;
 
-  // ---- global -> LDS DMA.  A slice of one operand is 256 rows x 32 k = 16 x 1 KB
-  // blocks; wave w moves blocks 4j + w (j = 0..3).  Inside a block, lane L writes
-  // LDS bytes [16 L, 16 L + 16): row 16*block + L/4, swizzled position L%4, which
-  // holds logical k-chunk (L%4) ^ ((row/4)%4) of that row.
-  typedef __attribute__((address_space(3))) void lds_t;
-  typedef __attribute__((address_space(3))) char lds_c;
+  // ---- global -> LDS DMA.  A slice of one operand is 256 rows x 64 k = 32 x 1 KB
+  // blocks; wave w moves blocks WAVES*j + w.  Inside a block, lane L writes LDS
+  // bytes [16 L, 16 L + 16): row 8*block + L/8, swizzled position L%8, which
+  // holds logical k-chunk (L%8) ^ ((row/2)%8) of that row.
   const __amdgpu_buffer_rsrc_t xres = make_rsrc(p.X, (uint32_t)((int64_t)p.M * p.ldx * 2));
-  uint32_t xoff[4], woff[4];
-  __amdgpu_buffer_rsrc_t wres[4];
+  uint32_t xoff[BLK], woff[BLK];
+  __amdgpu_buffer_rsrc_t wres[BLK];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int blk = 4 * j + wave;
-    const int row = blk * 16 + lane / 4;
-    const int c = (lane % 4) ^ ((row >> 2) & 3);
+  for (int j = 0; j < BLK; ++j) {
+    const int blk = WAVES * j + wave;
+    const int row = blk * 8 + lane / 8;
+    const int c = (lane % 8) ^ ((row >> 1) & 7);
     const int xr = m0 + row;
     xoff[j] = xr < p.M ? (uint32_t)(((int64_t)xr * p.ldx + c * 8) * 2) : CRF_OOB;
-    // weight rows: the 16 rows of a block sit in one 64-row group, inside one segment
+    // weight rows: the 8 rows of a block sit in one 64-row group, inside one segment
     const int wr = n0 + row;
     int lr0, local;
-    const int sg = segment_of<EPI>(p, min(n0 + blk * 16, p.N - 1), lr0);
+    const int sg = segment_of<EPI>(p, min(n0 + blk * 8, p.N - 1), lr0);
     const int seg_rows = EPI == EPI_QKV ? (sg == 0 ? p.seg1 : sg == 1 ? p.seg2 - p.seg1 : p.N - p.seg2)
                                         : (EPI == EPI_SWIGLU ? p.N / 2 : p.N);
     segment_of<EPI>(p, min(wr, p.N - 1), local);
@@ -110,22 +116,21 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(const GemmParams p) {
     woff[j] = wr < p.N ? (uint32_t)(((int64_t)local * p.K + c * 8) * 2) : CRF_OOB;
   }
   auto dma = [&](int k0, int stage) {
-    lds_c *dx = (lds_c *)(lds_x + stage * BM * BK);
-    lds_c *dw = (lds_c *)(lds_w + stage * BN * BK);
+    lds_char *dx = (lds_char *)(lds_x + stage * BM * BK);
+    lds_char *dw = (lds_char *)(lds_w + stage * BN * BK);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int blk = 4 * j + wave;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(xres, (lds_t *)(dx + blk * 1024), 16, xoff[j], (uint32_t)k0 * 2, 0, 0);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(wres[j], (lds_t *)(dw + blk * 1024), 16, woff[j], (uint32_t)k0 * 2, 0,
-                                               0);
+    for (int j = 0; j < BLK; ++j) {
+      const int blk = WAVES * j + wave;
+      dma16(xres, dx + blk * 1024, xoff[j], (uint32_t)k0 * 2);
+      dma16(wres[j], dw + blk * 1024, woff[j], (uint32_t)k0 * 2);
     }
   };
 
-  f32x16 acc[4][4];
+  f32x16 acc[4][NJ];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < NJ; ++j)
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
@@ -148,8 +153,8 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(const GemmParams p) {
         lbf[i] = as_bf16x8(v);
       }
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int m = min(m0 + wm * 128 + 32 * j + l32, p.M - 1);
+      for (int j = 0; j < NJ; ++j) {
+        const int m = min(m0 + wm * WTM + 32 * j + l32, p.M - 1);
         const bf16 *urow = p.U + (int64_t)m * p.ldu + k;
         // segments used by this wave: blocks 0,1 and 2,3 may differ (EPI_SWIGLU)
         const bf16x8 u01 = as_bf16x8(ld16(urow + p.ucol[seg[0]]));
@@ -160,67 +165,62 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(const GemmParams p) {
     }
   }
 
-  const int nk = p.K / BK;  // >= 2 (K is a multiple of 64)
-  auto frag = [&](int stage, int s, bf16x8 (&fa)[4], bf16x8 (&fb)[4]) {
+  const int nk = p.K / BK;
+  auto frag = [&](int stage, int s, bf16x8 (&fa)[4], bf16x8 (&fb)[NJ]) {
     const bf16 *sx = lds_x + stage * BM * BK;
     const bf16 *sw = lds_w + stage * BN * BK;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      fa[i] = as_bf16x8(ld16(sw + swz(wn * 128 + 32 * i + l32, 2 * s + g)));
-      fb[i] = as_bf16x8(ld16(sx + swz(wm * 128 + 32 * i + l32, 2 * s + g)));
-    }
+    for (int i = 0; i < 4; ++i) fa[i] = as_bf16x8(ld16(sw + swz(wn * 128 + 32 * i + l32, 2 * s + g)));
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) fb[j] = as_bf16x8(ld16(sx + swz(wm * WTM + 32 * j + l32, 2 * s + g)));
   };
-  // Wait for this wave's DMA of slice `kt` (later slices may stay in flight:
-  // 8 DMA instructions per slice), then a bare barrier publishes every wave's
-  // part.  Reads of earlier slices are complete (lgkmcnt(0)) before it, so a
-  // DMA issued after it may reuse their stage.
-  auto slice_ready = [&](int kt) {
-    const int later = min(nk - 1 - kt, STAGES - 2);
-    if (later >= 2)
+  auto mm = [&](bf16x8 (&fa)[4], bf16x8 (&fb)[NJ]) {
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) acc[i][j] = mfma32(fa[i], fb[j], acc[i][j]);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  // prologue: slices 0 and 1 in flight, slice 0 published, its step-0 fragments loaded
+  dma(0, 0);
+  if (nk > 1) {
+    dma(BK, 1);
+    if (DMA_PER_SLICE == 16)
       asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
-    else if (later == 1)
-      asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
     else
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-  };
-  // prologue: three slices in flight, slice 0 published, its step-0 fragments loaded
-#pragma unroll
-  for (int st = 0; st < STAGES - 1; ++st)
-    if (st < nk) dma(st * BK, st);
-  slice_ready(0);
-  bf16x8 a0[4], b0[4], a1[4], b1[4];
+      asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+  } else {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  }
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  bf16x8 a0[4], b0[NJ], a1[4], b1[NJ];
   frag(0, 0, a0, b0);
-  // Steady state per slice kt: [step-1 reads of kt, DMA of kt+3] -> step-0 MFMAs ->
-  // publish slice kt+1 -> [step-0 reads of kt+1] -> step-1 MFMAs.  Fragments are
-  // always read one MFMA group ahead, and the barrier sits between the groups.
+  // Per slice kt: four k-steps of MFMAs with the next step's fragments read
+  // ahead; before the last step, wait for slice kt+1 (own DMA, then a bare
+  // barrier publishing every wave's part and retiring all reads of slice kt),
+  // refill this stage with slice kt+2 and read slice kt+1's first fragments.
   for (int kt = 0; kt < nk; ++kt) {
-    const int stage = kt % STAGES;
-    frag(stage, 1, a1, b1);
-    if (kt + STAGES - 1 < nk) dma((kt + STAGES - 1) * BK, (kt + STAGES - 1) % STAGES);
-    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) acc[i][j] = mfma32(a0[i], b0[j], acc[i][j]);
-    __builtin_amdgcn_sched_barrier(0);
+    const int st = kt & 1;
+    frag(st, 1, a1, b1);
+    mm(a0, b0);
+    frag(st, 2, a0, b0);
+    mm(a1, b1);
+    frag(st, 3, a1, b1);
+    mm(a0, b0);
     if (kt + 1 < nk) {
-      slice_ready(kt + 1);
-      frag((kt + 1) % STAGES, 0, a0, b0);
+      asm volatile("s_waitcnt vmcnt(0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+      if (kt + 2 < nk) dma((kt + 2) * BK, st);
+      frag(st ^ 1, 0, a0, b0);
     }
-    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) acc[i][j] = mfma32(a1[i], b1[j], acc[i][j]);
-    __builtin_amdgcn_sched_barrier(0);
+    mm(a1, b1);
   }
 
   // ---- epilogues
   if (EPI == EPI_RESID) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int m = m0 + wm * 128 + 32 * j + l32;
+    for (int j = 0; j < NJ; ++j) {
+      const int m = m0 + wm * WTM + 32 * j + l32;
       if (m >= p.M) continue;
 #pragma unroll
       for (int i = 0; i < 4; ++i)
@@ -239,8 +239,8 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(const GemmParams p) {
   } else if (EPI == EPI_SWIGLU) {
     const int fbase = (n0 + wn * 128) / 2;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int m = m0 + wm * 128 + 32 * j + l32;
+    for (int j = 0; j < NJ; ++j) {
+      const int m = m0 + wm * WTM + 32 * j + l32;
       if (m >= p.M) continue;
 #pragma unroll
       for (int i = 0; i < 2; ++i)
@@ -266,8 +266,8 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(const GemmParams p) {
     const int head0 = local / HD;
     const bf16 *bias = p.bias[sg];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int m = m0 + wm * 128 + 32 * j + l32;
+    for (int j = 0; j < NJ; ++j) {
+      const int m = m0 + wm * WTM + 32 * j + l32;
       if (m >= p.M || fb >= p.N) continue;
       int64_t prow[HPW];
 #pragma unroll
@@ -319,31 +319,36 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_kernel(const GemmParams p) {
   }
 }
 
-template <int EPI, int HD>
+template <int EPI, int HD, int WAVES>
 hipError_t go(hipStream_t s, const GemmParams &p) {
   const int tiles = ((p.M + BM - 1) / BM) * ((p.N + BN - 1) / BN);
   const size_t lds = (size_t)STAGES * (BM + BN) * BK * sizeof(bf16);
   static bool attr_set = false;
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void *)gemm_bf16_kernel<EPI, HD>,
+    hipError_t e = hipFuncSetAttribute((const void *)gemm_bf16_kernel<EPI, HD, WAVES>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
     attr_set = true;
   }
-  hipLaunchKernelGGL((gemm_bf16_kernel<EPI, HD>), dim3(tiles), dim3(NT), lds, s, p);
+  hipLaunchKernelGGL((gemm_bf16_kernel<EPI, HD, WAVES>), dim3(tiles), dim3(64 * WAVES), lds, s, p);
   return hipGetLastError();
 }
+
+#ifndef CRF_GEMM_WAVES
+#define CRF_GEMM_WAVES 8
+#endif
 
 }  // namespace
 
 hipError_t launch_gemm_bf16(hipStream_t s, GemmEpi epi, int hd, const GemmParams &p) {
+  constexpr int W = CRF_GEMM_WAVES;
   if (p.M <= 0 || p.N <= 0) return hipSuccess;
   if (p.K % BK) return hipErrorInvalidValue;
   if ((int64_t)p.M * p.ldx * 2 >= (int64_t)CRF_OOB) return hipErrorInvalidValue;  // X must fit one buffer resource
   switch (epi) {
-    case EPI_RESID: return go<EPI_RESID, 128>(s, p);
-    case EPI_SWIGLU: return go<EPI_SWIGLU, 128>(s, p);
-    case EPI_QKV: return hd == 64 ? go<EPI_QKV, 64>(s, p) : go<EPI_QKV, 128>(s, p);
+    case EPI_RESID: return go<EPI_RESID, 128, W>(s, p);
+    case EPI_SWIGLU: return go<EPI_SWIGLU, 128, W>(s, p);
+    case EPI_QKV: return hd == 64 ? go<EPI_QKV, 64, W>(s, p) : go<EPI_QKV, 128, W>(s, p);
   }
   return hipErrorInvalidValue;
 }
