@@ -9,8 +9,9 @@ pages), inputs resident in HBM before the timed region.  Prints one JSON line.
 
 Other workloads (one JSON line each): tiny_f32, qwen15b_4k, qwen7b_16k_suffix
 (the 24-layer affected suffix), qwen15b_mixed8 (8 ragged stale caches through
-the batched call) and drift (crf_layer_drift over 28 layers and 4 stored
-adapter versions at 1.5B shapes).
+the batched call), drift (crf_layer_drift over 28 layers and 4 stored
+adapter versions at 1.5B shapes) and copy (a 1 GiB elementwise pass that
+calibrates the HBM byte counters).
 """
 from __future__ import annotations
 
@@ -102,6 +103,8 @@ def main():
         return bench_drift(args)
     if args.workload == "qwen15b_mixed8":
         return bench_mixed(args)
+    if args.workload == "copy":
+        return bench_copy(args)
     wl = syn.WORKLOADS[args.workload]
     dims = wl.dims
     win = wl.window
@@ -306,6 +309,25 @@ def bench_drift(args):
                      "traffic": None},
         "kernels": {k: {"avg_ms": round(v[0] / v[1], 4), "launches": v[1]} for k, v in timing.items() if v[1]},
     }
+    print(json.dumps(out), flush=True)
+
+
+def bench_copy(args):
+    """A plain elementwise pass of known size (1 GiB read, 1 GiB written): the
+    calibration point that turns the FETCH_SIZE / WRITE_SIZE counters into
+    bytes for the traffic figure of the roofline."""
+    import torch
+    n = 1 << 28                                    # fp32 elements: 1 GiB
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    elapsed, _ = _timed(lambda: torch.neg(src, out=dst), args.steps, args.warmup)
+    bytes_per = 2 * 4 * n
+    out = {"metric": "device copy bandwidth (elementwise pass, 1 GiB in + 1 GiB out)",
+           "value": round(bytes_per * args.steps / elapsed / 1e9, 1), "unit": "GB/s", "n_gpus": 1,
+           "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(1e3 * elapsed / args.steps, 4),
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+           "config": {"workload": "copy: 2^28 fp32 elements read and written once per step",
+                      "bytes_read": 4 * n, "bytes_written": 4 * n}}
     print(json.dumps(out), flush=True)
 
 
