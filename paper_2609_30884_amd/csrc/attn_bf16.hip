@@ -2,23 +2,34 @@
 // the paged cache (flash-style: K/V tiles staged in LDS, online softmax).
 //
 // Workgroup = one query head x 128 queries: 4 waves of 32 queries, two
-// workgroups per CU (two waves per SIMD, so one wave's softmax overlaps the
-// other's MFMAs).  Each wave computes S^T = K Q^T (keys on MFMA rows, queries
-// on columns), so a lane owns one query and 16 of the 32 keys of a block: the
-// online-softmax max and sum are in-lane plus one exchange with lane^32.  The
-// probabilities feed O^T = V^T P^T straight from the S accumulators: the 8
-// consecutive accumulator registers of a key half-block are the 8 k-slots a
-// lane supplies, provided the V^T operand uses the same key order (keys
-// 8*ii + 4*(lane/32) + jj).  V is transposed into LDS ([hd][key]) once per
-// tile; K is stored [key][hd] with XOR-swizzled 16-byte chunks.
+// workgroups per CU (two waves per SIMD from independent workgroups, so one
+// wave's softmax overlaps the other's MFMAs).  Each wave computes S^T = K Q^T
+// (keys on MFMA rows, queries on columns), so a lane owns one query and 16 of
+// the 32 keys of a block: the online-softmax max and sum are in-lane plus one
+// exchange with lane^32.  The probabilities feed O^T = V^T P^T straight from
+// the S accumulators: the 8 accumulator registers of a key half-block are the
+// 8 k-slots a lane supplies, so the V^T operand takes keys in the same order
+// (slots 0-3: keys 4*(lane/32) + 0..3, slots 4-7: the same plus 8).
 //
-// K/V come from the pages through buffer loads.  The workgroup's page bases
-// are staged in LDS once (validated there) and read per tile from LDS, so no
-// vector-memory wait ever sits between a tile's prefetch and its use; the page
-// base goes into the scalar offset, and keys past the prefix or on a rejected
-// page get an out-of-range offset, which the hardware returns as zero.  The running max is
-// only moved (and O rescaled) when a score exceeds it by more than 2^8 in
-// probability, so most tiles skip the rescale; probabilities stay below 2^8.
+// K and V tiles go from the pages straight into LDS (buffer loads with an LDS
+// destination, no register staging), both in their natural [key][hd] layout
+// with XOR-swizzled 16-byte chunks.  The V^T operand is read with the gfx950
+// LDS transpose read: within each 16-lane group, lane 4r+c points at 4
+// consecutive hd values of key row r, and lane j receives hd column j of the 4
+// rows.  A two-stage ring lets the loads of tile i+1 run under the MFMAs of
+// tile i, with one barrier per tile.
+//
+// The workgroup's page bases are staged in LDS once (validated there); a key
+// past the prefix or on a rejected page gets an out-of-range buffer offset,
+// which the hardware returns as zero.  The running max is only moved (and O
+// rescaled) when a score exceeds it by more than 2^8 in probability, so most
+// tiles skip the rescale; probabilities stay below 2^8.
+//
+// Launch order: workgroup b runs on XCD b % 8.  When the KV-head count divides
+// 8, each XCD serves one KV head and every R-th query block (R = 8 / n_kv),
+// longest causal rows first, with the G query heads of that KV head adjacent:
+// the work per XCD is balanced and the heads that share K/V tiles run side by
+// side on one L2.
 #include <math.h>
 
 #include "kernels.hpp"
@@ -28,55 +39,81 @@ namespace {
 
 constexpr int BQ = 128;   // queries per workgroup
 constexpr int BKV = 64;   // keys per tile
-constexpr int VT_LD = BKV + 4;
 constexpr float RESCALE_THRESHOLD = 8.0f;  // log2 units
-constexpr int PGCAP = 2048;  // page bases staged in LDS at a time (32768 keys of 16-token pages)
+constexpr int PGCAP = 2048;  // page bases staged in LDS at a time
 
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+
+// 16-byte chunk slot of chunk c in K row r: conflict-free 16-byte fragment reads.
 template <int HD>
-CRF_DEV int kswz(int row, int chunk) {
-  if (HD == 128) return row * HD + ((chunk ^ (row & 15)) << 3);
-  return row * HD + ((chunk ^ ((row >> 1) & 7)) << 3);
+CRF_DEV int kslot(int r, int c) {
+  return c ^ (r & (HD / 8 - 1));
+}
+// Chunk slot in V row r: every transpose read (4 rows x 32 bytes per 16 lanes,
+// 4 rows x 64 bytes per 32 lanes) lands on distinct banks.
+template <int HD>
+CRF_DEV int vslot(int r, int c) {
+  if (HD == 128) return c ^ ((0xCA60 >> (4 * (r & 3))) & 15);
+  return c ^ (2 * (r & 3));
 }
 
 CRF_DEV float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-// Byte offset of the first key of page `p` for this KV head, or CRF_OOB.
+CRF_DEV s16x4 ld_tr(const bf16 *p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(const __attribute__((address_space(3))) void *)p);
+}
+
+// Byte offset of the first key of logical page p for this KV head, or CRF_OOB.
 struct PageMap {
   const int32_t *bt;
-  int n_pages, page_size, M;
+  int n_pages;
   uint32_t page_bytes, head_bytes;
   int *err;
-  CRF_DEV uint32_t base(int tok) const {
-    if (tok >= M) return CRF_OOB;
-    const int p = bt[tok / page_size];
-    if (p < 0 || p >= n_pages) {
+  CRF_DEV uint32_t base(int p) const {
+    const int q = bt[p];
+    if (q < 0 || q >= n_pages) {
       atomicOr(err, (int)CRF_DEVERR_BLOCK_TABLE);
       return CRF_OOB;
     }
-    return (uint32_t)p * page_bytes + head_bytes;
+    return (uint32_t)q * page_bytes + head_bytes;
   }
 };
 
-template <int HD, bool PAGE16>
+// PS: page size when fixed at compile time (16), 0 = runtime kv.page_size.
+// XCD: balanced per-XCD KV-head mapping (R = 8 / nkv XCDs per KV head).
+template <int HD, int PS>
 __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16 *__restrict__ Q, PagedKV kv,
                                                            bf16 *__restrict__ O, int M, int nq, int nkv,
-                                                           uint32_t pool_bytes) {
-  constexpr int CH = HD / 8;           // 16-byte chunks per K row
-  constexpr int KS = HD / 16;          // MFMA k-steps for S
-  constexpr int HB = HD / 32;          // 32-row hd blocks of O^T
-  constexpr int KCH = BKV * CH / 256;  // K chunks per thread per tile (one key each)
-  constexpr int VCH = CH / 8;          // V hd-chunks per thread (each for 2 keys)
-  constexpr int KROWS = 256 / CH;      // keys covered by one K chunk round
-  __shared__ __align__(16) bf16 ks[2][BKV * HD];
-  __shared__ __align__(16) bf16 vt[2][HD * VT_LD];
-  __shared__ uint32_t pgbase[PAGE16 ? PGCAP : 1];
+                                                           uint32_t pool_bytes, int xcd_r) {
+  constexpr int CH = HD / 8;             // 16-byte chunks per row
+  constexpr int KS = HD / 16;            // MFMA k-steps for S
+  constexpr int HB = HD / 32;            // 32-row hd blocks of O^T
+  constexpr int RPI = 64 / CH;           // rows per 64-lane load instruction
+  constexpr int IPW = BKV / RPI / 4;     // load instructions per wave per tile (each of K and V)
+  constexpr int TILE = BKV * HD;         // elements per K (or V) tile
+  // one array per stage and operand, so the compiler sees that loads into one
+  // stage never alias reads of the other
+  __shared__ __align__(16) bf16 ks0[TILE], ks1[TILE], vs0[TILE], vs1[TILE];
+  __shared__ uint32_t pgbase[PGCAP];
 
   const int nqb = (M + BQ - 1) / BQ;
-  const int t = xcd_remap(blockIdx.x, gridDim.x);
-  const int head = t % nq;
-  const int qblk = nqb - 1 - t / nq;  // longest causal rows first
-  const int g_kv = head / (nq / nkv);
-  const int tid = threadIdx.x, lane = tid % 64, wave = tid / 64;
+  const int group = nq / nkv;
+  int head, qblk;
+  if (xcd_r > 0) {
+    const int x = blockIdx.x % 8, j = blockIdx.x / 8;
+    const int qi = j / group;
+    head = (x / xcd_r) * group + j % group;
+    qblk = nqb - 1 - (qi * xcd_r + x % xcd_r);
+    if (qblk < 0) return;  // padding of the per-XCD lists (uniform per workgroup)
+  } else {
+    head = blockIdx.x % nq;
+    qblk = nqb - 1 - blockIdx.x / nq;  // longest causal rows first
+  }
+  const int g_kv = head / group;
+  const int ps = PS > 0 ? PS : kv.page_size;
+  const int tid = threadIdx.x, lane = tid % 64;
+  const int wave = __builtin_amdgcn_readfirstlane(tid / 64);
   const int g = lane / 32, l32 = lane % 32;
   const int q0 = qblk * BQ;
   const int q0w = q0 + wave * 32;
@@ -92,73 +129,38 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16 *__restric
 
   const __amdgpu_buffer_rsrc_t kres = make_rsrc(kv.k, pool_bytes);
   const __amdgpu_buffer_rsrc_t vres = make_rsrc(kv.v, pool_bytes);
-  const PageMap pm{kv.block_table, kv.n_pages, kv.page_size, M, (uint32_t)(kv.page_stride * 2),
-                   (uint32_t)(g_kv * kv.page_size * HD * 2), kv.err};
+  const PageMap pm{kv.block_table, kv.n_pages, (uint32_t)(kv.page_stride * 2), (uint32_t)(g_kv * ps * HD * 2),
+                   kv.err};
 
-  // per-thread key/chunk coordinates inside a tile
-  const int kkey = tid / CH, kc = tid % CH;          // K: keys kkey + KROWS*i, chunk kc
-  const int vkp = tid % 32, vc = tid / 32;           // V: keys 2vkp, 2vkp+1, chunks vc + 8i
+  const int last_key = min(q0 + BQ, M) - 1;
+  const int ntiles = last_key / BKV + 1;
+  const int n_pages_needed = last_key / ps + 1;
 
-  // Page bases (16-token pages) staged in LDS: pgbase[i] = base of page
-  // pg_first + i.  A refill happens between barriers, never while read.
+  // pgbase[i] = base of logical page pg_first + i; refilled only between barriers.
   int pg_first = 0;
-  auto fill_pages = [&](int first, int n_needed) {
+  auto fill_pages = [&](int first) {
     pg_first = first;
-    for (int i = tid; i < min(PGCAP, n_needed - first); i += 256) pgbase[i] = pm.base((first + i) * 16);
-  };
-  auto tile_pages = [&](int kt0, uint32_t (&pb)[4]) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      pb[i] = PAGE16 ? (uint32_t)__builtin_amdgcn_readfirstlane((int)pgbase[kt0 / 16 + i - pg_first]) : 0u;
+    for (int i = tid; i < min(PGCAP, n_pages_needed - first); i += 256) pgbase[i] = pm.base(first + i);
   };
 
-  u32x4 pk[KCH], pv[2 * VCH];
-  auto gload = [&](int kt0, const uint32_t (&pb)[4]) {
+  // This lane's row and chunk in each of the wave's load instructions.
+  const int lrow = lane / CH, lslot = lane % CH;
+  auto dma = [&](int kt0, bf16 *kdst, bf16 *vdst) {
+    uint32_t b[IPW];
 #pragma unroll
-    for (int i = 0; i < KCH; ++i) {
-      const int key = kkey + KROWS * i;
-      const int tok = kt0 + key;
-      uint32_t soff, voff;
-      if (PAGE16) {
-        // the page (key / 16) is a per-lane choice among the tile's 4 uniform bases
-        const uint32_t b = pb[key / 16];
-        soff = 0;
-        voff = (tok < M && b != CRF_OOB) ? b + (uint32_t)(((key & 15) * HD + kc * 8) * 2) : CRF_OOB;
-      } else {
-        soff = 0;
-        const uint32_t b = pm.base(tok);
-        voff = b == CRF_OOB ? CRF_OOB : b + (uint32_t)(((tok % kv.page_size) * HD + kc * 8) * 2);
-      }
-      pk[i] = bld16(kres, voff, soff);
+    for (int i = 0; i < IPW; ++i) {
+      const int tok = kt0 + wave * (BKV / 4) + RPI * i + lrow;
+      b[i] = pgbase[min(max(tok / ps - pg_first, 0), PGCAP - 1)];  // clamped: used only when tok < M
     }
 #pragma unroll
-    for (int e = 0; e < 2; ++e) {
-      const int key = 2 * vkp + e;
-      const int tok = kt0 + key;
-      uint32_t base;
-      if (PAGE16) {
-        const uint32_t b = pb[key / 16];
-        base = (tok < M && b != CRF_OOB) ? b + (uint32_t)((key & 15) * HD * 2) : CRF_OOB;
-      } else {
-        const uint32_t b = pm.base(tok);
-        base = b == CRF_OOB ? CRF_OOB : b + (uint32_t)((tok % kv.page_size) * HD * 2);
-      }
-#pragma unroll
-      for (int i = 0; i < VCH; ++i) pv[2 * i + e] = bld16(vres, base == CRF_OOB ? CRF_OOB : base + (vc + 8 * i) * 16, 0);
-    }
-  };
-  auto lstore = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < KCH; ++i) st16(&ks[buf][kswz<HD>(kkey + KROWS * i, kc)], pk[i]);
-#pragma unroll
-    for (int i = 0; i < VCH; ++i) {
-      const int c = vc + 8 * i;
-      const bf16x8 v0 = as_bf16x8(pv[2 * i]), v1 = as_bf16x8(pv[2 * i + 1]);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        bf16x2 pr = {v0[e], v1[e]};
-        *reinterpret_cast<bf16x2 *>(&vt[buf][(c * 8 + e) * VT_LD + 2 * vkp]) = pr;
-      }
+    for (int i = 0; i < IPW; ++i) {
+      const int row = wave * (BKV / 4) + RPI * i + lrow;  // key within the tile
+      const int tok = kt0 + row;
+      const bool ok = tok < M && b[i] != CRF_OOB;
+      const uint32_t rowoff = b[i] + (uint32_t)((tok % ps) * HD * 2);
+      const int ldsoff = (wave * (BKV / 4) + RPI * i) * HD;  // wave-uniform first row of this instruction
+      dma16(kres, (lds_char *)(kdst + ldsoff), ok ? rowoff + (uint32_t)(kslot<HD>(row, lslot) * 16) : CRF_OOB, 0);
+      dma16(vres, (lds_char *)(vdst + ldsoff), ok ? rowoff + (uint32_t)(vslot<HD>(row, lslot) * 16) : CRF_OOB, 0);
     }
   };
 
@@ -170,102 +172,103 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16 *__restric
   float m_run = -INFINITY, l_run = 0.f;
   const float c2 = 1.4426950408889634f / sqrtf((float)HD);  // log2(e) / sqrt(hd)
 
-  const int last_key = min(q0 + BQ, M) - 1;
-  const int ntiles = last_key / BKV + 1;
-  const int n_pages_needed = ntiles * (BKV / 16);
-  if (PAGE16) {
-    fill_pages(0, n_pages_needed);
-    __syncthreads();
-  }
-  {
-    uint32_t pb[4];
-    tile_pages(0, pb);
-    gload(0, pb);
-  }
-  lstore(0);
-  __syncthreads();
-  for (int it = 0; it < ntiles; ++it) {
-    const int buf = it & 1;
+  // Transpose-read coordinates: 16-lane group gq covers hd 16*(gq&1) .. +15 of a
+  // 32-row block and key rows 4*(gq>>1) + r; lane 4r + c reads hd chunk c*4.
+  const int tr_r = (lane % 16) / 4, tr_c = lane % 4, tr_g = lane / 16;
+  const int tr_key = 4 * (tr_g >> 1) + tr_r;            // + key half-block base (+8 for slots 4-7)
+  const int tr_hd = 16 * (tr_g & 1) + 4 * tr_c;         // + 32*b
+
+  // One tile: wait for its loads, publish them, start the next tile's loads
+  // into the other stage, then compute.
+  auto tile = [&](int it, const bf16 *kt, const bf16 *vt, bf16 *kn, bf16 *vn) {
     const int kt0 = it * BKV;
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
     if (it + 1 < ntiles) {
-      if (PAGE16 && (kt0 + BKV) / 16 + 4 > pg_first + PGCAP) {
-        // every wave is past the previous barrier, so nobody reads pgbase now
-        fill_pages((kt0 + BKV) / 16, n_pages_needed);
+      const int next_last_page = (min(kt0 + 2 * BKV, M) - 1) / ps;
+      if (next_last_page >= pg_first + PGCAP) {
+        fill_pages((kt0 + BKV) / ps);
         __syncthreads();
       }
-      uint32_t pb[4];
-      tile_pages(kt0 + BKV, pb);
-      gload(kt0 + BKV, pb);
+      dma(kt0 + BKV, kn, vn);
     }
-    if (kt0 <= q0w + 31) {  // some key of this tile is visible to this wave
-      f32x16 sacc[2];
+    if (kt0 > q0w + 31) return;  // every key of this tile is in this wave's future
+    f32x16 sacc[2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) sacc[kb][v] = 0.f;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        const int r = kb * 32 + l32;
+        const bf16x8 kf = as_bf16x8(ld16(kt + r * HD + kslot<HD>(r, 2 * s + g) * 8));
+        sacc[kb] = mfma32(kf, qf[s], sacc[kb]);
+      }
+    }
+    // causal mask (also hides keys >= M, which are always > qi for valid qi)
+    if (kt0 + BKV - 1 > q0w) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) sacc[kb][v] = 0.f;
-#pragma unroll
-      for (int s = 0; s < KS; ++s) {
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
-          const bf16x8 kf = as_bf16x8(ld16(&ks[buf][kswz<HD>(kb * 32 + l32, 2 * s + g)]));
-          sacc[kb] = mfma32(kf, qf[s], sacc[kb]);
+        for (int v = 0; v < 16; ++v) {
+          const int key = kt0 + kb * 32 + 8 * (v / 4) + 4 * g + (v % 4);
+          if (key > qi) sacc[kb][v] = -INFINITY;
         }
-      }
-      // causal mask (also hides keys >= M, which are always > qi for valid qi)
-      if (kt0 + BKV - 1 > q0w) {
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            const int key = kt0 + kb * 32 + 8 * (v / 4) + 4 * g + (v % 4);
-            if (key > qi) sacc[kb][v] = -INFINITY;
-          }
-      }
-      float mx = -INFINITY;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sacc[kb][v]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * c2;
-      // move the reference max only when a probability would exceed 2^8
-      const bool grow = mx > m_run + RESCALE_THRESHOLD;
-      if (__builtin_amdgcn_ballot_w64(grow)) {
-        const float m_new = grow ? mx : m_run;
-        const float alpha = fast_exp2(m_run - m_new);  // 0 on the first visible tile
-        m_run = m_new;
-        l_run *= alpha;
-#pragma unroll
-        for (int b = 0; b < HB; ++b) oacc[b] *= alpha;
-      }
-      float psum = 0.f;
-      bf16x8 pf[2][2];
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int hh = 0; hh < 2; ++hh)
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const float p = fast_exp2(fmaf(sacc[kb][8 * hh + e], c2, -m_run));
-            psum += p;
-            pf[kb][hh][e] = f2bf(p);
-          }
-      l_run += psum;
-      // O^T[hd, q] += V^T[hd, keys] P^T[keys, q]
-#pragma unroll
-      for (int b = 0; b < HB; ++b) {
-        const bf16 *vrow = &vt[buf][(b * 32 + l32) * VT_LD];
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-          for (int hh = 0; hh < 2; ++hh) {
-            const int kbase = kb * 32 + 16 * hh + 4 * g;
-            const u32x2 lo = ld8(vrow + kbase), hi = ld8(vrow + kbase + 8);
-            oacc[b] = mfma32(as_bf16x8(u32x4{lo[0], lo[1], hi[0], hi[1]}), pf[kb][hh], oacc[b]);
-          }
-      }
     }
-    if (it + 1 < ntiles) lstore(buf ^ 1);
-    __syncthreads();
+    float mx = -INFINITY;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sacc[kb][v]);
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * c2;
+    // move the reference max only when a probability would exceed 2^8
+    const bool grow = mx > m_run + RESCALE_THRESHOLD;
+    if (__builtin_amdgcn_ballot_w64(grow)) {
+      const float m_new = grow ? mx : m_run;
+      const float alpha = fast_exp2(m_run - m_new);  // 0 on the first visible tile
+      m_run = m_new;
+      l_run *= alpha;
+#pragma unroll
+      for (int b = 0; b < HB; ++b) oacc[b] *= alpha;
+    }
+    float psum = 0.f;
+    bf16x8 pf[2][2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float p = fast_exp2(fmaf(sacc[kb][8 * hh + e], c2, -m_run));
+          psum += p;
+          pf[kb][hh][e] = f2bf(p);
+        }
+    l_run += psum;
+    // O^T[hd, q] += V^T[hd, keys] P^T[keys, q]
+#pragma unroll
+    for (int b = 0; b < HB; ++b) {
+      const int hd = 32 * b + tr_hd;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh) {
+          const int r0 = kb * 32 + 16 * hh + tr_key, r1 = r0 + 8;
+          const s16x4 lo = ld_tr(vt + r0 * HD + vslot<HD>(r0, hd / 8) * 8 + hd % 8);
+          const s16x4 hi = ld_tr(vt + r1 * HD + vslot<HD>(r1, hd / 8) * 8 + hd % 8);
+          const s16x4 lohi[2] = {lo, hi};
+          oacc[b] = mfma32(__builtin_bit_cast(bf16x8, lohi), pf[kb][hh], oacc[b]);
+        }
+    }
+  };
+
+  fill_pages(0);
+  __syncthreads();
+  dma(0, ks0, vs0);
+  for (int it = 0; it < ntiles; it += 2) {
+    tile(it, ks0, vs0, ks1, vs1);
+    if (it + 1 < ntiles) tile(it + 1, ks1, vs1, ks0, vs0);
   }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
@@ -285,12 +288,17 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16 *__restric
 template <int HD>
 void launch(hipStream_t s, const bf16 *Q, const PagedKV &kv, bf16 *O, int M, int nq, int nkv, uint32_t pool_bytes) {
   const int nqb = (M + BQ - 1) / BQ;
+  int xcd_r = 0, grid = nqb * nq;
+  if (nkv <= 8 && 8 % nkv == 0) {
+    xcd_r = 8 / nkv;
+    grid = 8 * (nq / nkv) * ((nqb + xcd_r - 1) / xcd_r);
+  }
   if (kv.page_size == 16)
-    hipLaunchKernelGGL((attn_bf16_kernel<HD, true>), dim3(nqb * nq), dim3(256), 0, s, Q, kv, O, M, nq, nkv,
-                       pool_bytes);
+    hipLaunchKernelGGL((attn_bf16_kernel<HD, 16>), dim3(grid), dim3(256), 0, s, Q, kv, O, M, nq, nkv, pool_bytes,
+                       xcd_r);
   else
-    hipLaunchKernelGGL((attn_bf16_kernel<HD, false>), dim3(nqb * nq), dim3(256), 0, s, Q, kv, O, M, nq, nkv,
-                       pool_bytes);
+    hipLaunchKernelGGL((attn_bf16_kernel<HD, 0>), dim3(grid), dim3(256), 0, s, Q, kv, O, M, nq, nkv, pool_bytes,
+                       xcd_r);
 }
 
 }  // namespace

@@ -118,6 +118,28 @@ def test_bf16_window_parity(name, n, seed):
     _untouched(case, set(kv))
 
 
+@pytest.mark.parametrize("page_size,hd,nq,nkv,n", [
+    (8, 128, 12, 2, 700),    # runtime page size; two KV heads (four XCDs per KV head)
+    (1, 64, 12, 6, 300),     # one-token pages, head_dim 64, six KV heads (plain launch order)
+    (32, 64, 8, 2, 1100),    # 32-token pages, head_dim 64
+])
+def test_bf16_page_sizes_and_head_shapes(page_size, hd, nq, nkv, n):
+    """Paged attention and the K/V-writing epilogue with page sizes other than
+    16, head_dim 64 and KV-head counts that do and do not divide the XCD count."""
+    import dataclasses
+    from synthetic.device import build_case
+    wl = dataclasses.replace(syn.WORKLOADS["qwen15b_4k"], page_size=page_size).with_dims(
+        n_layers=4, d_model=768, n_q_heads=nq, n_kv_heads=nkv, head_dim=hd, d_ffn=2048).with_window(
+        n_tokens=n, l0=1, h=2)
+    print(f"[case] page_size={page_size} hd={hd} nq={nq} nkv={nkv} n={n}", flush=True)
+    case = build_case(wl, 11)
+    run_gpu_window(case)
+    torch.cuda.synchronize()
+    out, kv = oracle_window(case)
+    assert_window_parity(case, out, kv, label=f"ps={page_size} hd={hd} {nq}/{nkv} n={n}")
+    _untouched(case, set(kv))
+
+
 def test_bf16_qkv_bias_and_rank8():
     """Optional q/k/v biases and a rank-8 adapter on the bf16 path."""
     from synthetic.device import build_case
