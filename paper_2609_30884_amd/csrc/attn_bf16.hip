@@ -143,24 +143,59 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16 *__restric
     for (int i = tid; i < min(PGCAP, n_pages_needed - first); i += 256) pgbase[i] = pm.base(first + i);
   };
 
-  // This lane's row and chunk in each of the wave's load instructions.
+  // This lane's row and chunk in each of the wave's load instructions.  A wave
+  // loads 16 consecutive rows (keys) of the tile; the in-page part of each
+  // lane's offset (row in the page, swizzled chunk) is fixed for the kernel
+  // when the page size is a multiple of 16.
   const int lrow = lane / CH, lslot = lane % CH;
+  uint32_t koff[IPW], voff[IPW];
+#pragma unroll
+  for (int i = 0; i < IPW; ++i) {
+    const int row = RPI * i + lrow;  // row within the wave's 16
+    koff[i] = (uint32_t)(row * HD * 2 + kslot<HD>(row, lslot) * 16);
+    voff[i] = (uint32_t)(row * HD * 2 + vslot<HD>(row, lslot) * 16);
+  }
   auto dma = [&](int kt0, bf16 *kdst, bf16 *vdst) {
-    uint32_t b[IPW];
+    const int wrow0 = kt0 + wave * (BKV / 4);  // first key of this wave's 16 rows
+    if (PS > 0 && PS % 16 == 0) {
+      // the wave's 16 rows share one page: one uniform base (CRF_OOB plus an
+      // in-page offset stays out of range, pool sizes being below 2^31)
+      const int pidx = min(max(wrow0 / PS - pg_first, 0), PGCAP - 1);
+      const uint32_t b =
+          (uint32_t)__builtin_amdgcn_readfirstlane((int)pgbase[pidx]) + (uint32_t)((wrow0 % PS) * HD * 2);
+      if (wrow0 + BKV / 4 <= M) {  // uniform: all 16 rows inside the prefix
 #pragma unroll
-    for (int i = 0; i < IPW; ++i) {
-      const int tok = kt0 + wave * (BKV / 4) + RPI * i + lrow;
-      b[i] = pgbase[min(max(tok / ps - pg_first, 0), PGCAP - 1)];  // clamped: used only when tok < M
-    }
+        for (int i = 0; i < IPW; ++i) {
+          const int ldsoff = (wave * (BKV / 4) + RPI * i) * HD;  // wave-uniform first row of this instruction
+          dma16(kres, (lds_char *)(kdst + ldsoff), b + koff[i], 0);
+          dma16(vres, (lds_char *)(vdst + ldsoff), b + voff[i], 0);
+        }
+      } else {
 #pragma unroll
-    for (int i = 0; i < IPW; ++i) {
-      const int row = wave * (BKV / 4) + RPI * i + lrow;  // key within the tile
-      const int tok = kt0 + row;
-      const bool ok = tok < M && b[i] != CRF_OOB;
-      const uint32_t rowoff = b[i] + (uint32_t)((tok % ps) * HD * 2);
-      const int ldsoff = (wave * (BKV / 4) + RPI * i) * HD;  // wave-uniform first row of this instruction
-      dma16(kres, (lds_char *)(kdst + ldsoff), ok ? rowoff + (uint32_t)(kslot<HD>(row, lslot) * 16) : CRF_OOB, 0);
-      dma16(vres, (lds_char *)(vdst + ldsoff), ok ? rowoff + (uint32_t)(vslot<HD>(row, lslot) * 16) : CRF_OOB, 0);
+        for (int i = 0; i < IPW; ++i) {
+          const int ldsoff = (wave * (BKV / 4) + RPI * i) * HD;
+          const bool in = wrow0 + RPI * i + lrow < M;
+          dma16(kres, (lds_char *)(kdst + ldsoff), in ? b + koff[i] : CRF_OOB, 0);
+          dma16(vres, (lds_char *)(vdst + ldsoff), in ? b + voff[i] : CRF_OOB, 0);
+        }
+      }
+    } else {
+      uint32_t b[IPW];
+#pragma unroll
+      for (int i = 0; i < IPW; ++i) {
+        const int tok = wrow0 + RPI * i + lrow;
+        b[i] = pgbase[min(max(tok / ps - pg_first, 0), PGCAP - 1)];  // clamped: used only when tok < M
+      }
+#pragma unroll
+      for (int i = 0; i < IPW; ++i) {
+        const int row = wave * (BKV / 4) + RPI * i + lrow;  // key within the tile
+        const int tok = kt0 + row;
+        const bool ok = tok < M && b[i] != CRF_OOB;
+        const uint32_t rowoff = b[i] + (uint32_t)((tok % ps) * HD * 2);
+        const int ldsoff = (wave * (BKV / 4) + RPI * i) * HD;
+        dma16(kres, (lds_char *)(kdst + ldsoff), ok ? rowoff + (uint32_t)(kslot<HD>(row, lslot) * 16) : CRF_OOB, 0);
+        dma16(vres, (lds_char *)(vdst + ldsoff), ok ? rowoff + (uint32_t)(vslot<HD>(row, lslot) * 16) : CRF_OOB, 0);
+      }
     }
   };
 
@@ -198,14 +233,25 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16 *__restric
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int v = 0; v < 16; ++v) sacc[kb][v] = 0.f;
-#pragma unroll
-    for (int s = 0; s < KS; ++s) {
+    // K fragments are read two k-steps ahead of the MFMAs that use them (the
+    // scheduling barriers keep the compiler from regrouping them)
+    bf16x8 kf[3][2];
+    auto kread = [&](int s, bf16x8 (&f)[2]) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
         const int r = kb * 32 + l32;
-        const bf16x8 kf = as_bf16x8(ld16(kt + r * HD + kslot<HD>(r, 2 * s + g) * 8));
-        sacc[kb] = mfma32(kf, qf[s], sacc[kb]);
+        f[kb] = as_bf16x8(ld16(kt + r * HD + kslot<HD>(r, 2 * s + g) * 8));
       }
+    };
+    kread(0, kf[0]);
+    kread(1, kf[1]);
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      if (s + 2 < KS) kread(s + 2, kf[(s + 2) % 3]);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) sacc[kb] = mfma32(kf[s % 3][kb], qf[s], sacc[kb]);
+      __builtin_amdgcn_sched_barrier(0);
     }
     // causal mask (also hides keys >= M, which are always > qi for valid qi)
     if (kt0 + BKV - 1 > q0w) {
