@@ -26,6 +26,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 METRIC = "recomputed token-layers/sec and ms per 16K-token window (7B-shape); MFMA util"
+SHAPE_NAME = {3584: "Qwen2.5-7B", 1536: "Qwen2.5-1.5B"}
 PEAK_BF16 = 2.5e15      # MI355X dense bf16 MFMA, FLOP/s
 PEAK_HBM = 8.0e12       # bytes/s
 
@@ -63,9 +64,13 @@ def cpu_baseline(case, n_sample: int):
     window; returns token-layers/s, seconds and thread count."""
     import numpy as np
     from oracle import oracle as O
+    blas = "unknown"
     try:
         from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+        info = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+        threads = max([i.get("num_threads", 1) for i in info] or [1])
+        if info:
+            blas = f"{info[0].get('internal_api')} {info[0].get('version')}"
     except Exception:
         threads = len(os.sched_getaffinity(0))
     win = case.window
@@ -73,7 +78,43 @@ def cpu_baseline(case, n_sample: int):
     t0 = time.perf_counter()
     O.recompute_window(h0, case.weights, case.lora, win.l0, win.h, case.dims, case.wl.lora_scale)
     dt = time.perf_counter() - t0
-    return n_sample * win.h / dt, dt, threads
+    return n_sample * win.h / dt, dt, threads, blas
+
+
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def tail_skipped_flops(dims, n, rank, targets):
+    """Algorithmic FLOP the K/V-only last layer does not run: Q, attention, O
+    and the MLP (with their adapter deltas)."""
+    d, dq, f = dims.d_model, dims.dq, dims.d_ffn
+    gemm = 2 * n * (d * dq + dq * d + d * 2 * f + f * d)
+    lora = sum(2 * n * rank * sum(dims.target_shape(t)) for t in targets if t in ("q", "o", "gate", "up", "down"))
+    attn = 2 * 2 * dims.n_q_heads * dims.head_dim * (n * (n + 1) // 2)
+    return gemm + lora + attn
+
+
+def hbm_bytes(dims, n, h, rank, targets, kv_tail):
+    """Algorithmic HBM bytes per window of the HBM-bound kernel classes (each
+    tensor read or written once): RMSNorm (bf16 or fp32 residual in, bf16 out)
+    and the skinny LoRA-down passes (activation in, rank columns out)."""
+    d, dq, f = dims.d_model, dims.dq, dims.d_ffn
+    norm = n * d * (2 + 4 + 2) + (2 * h - 1 - (1 if kv_tail else 0)) * n * d * (4 + 2)
+    r3 = 3 * rank * 2
+    per_layer = {"qkv": n * d * 2 + n * r3, "o": n * dq * 2 + n * r3, "gateup": n * d * 2 + n * r3,
+                 "down": n * f * 2 + n * r3}
+    has = {"qkv": any(t in targets for t in "qkv"), "o": "o" in targets,
+           "gateup": "gate" in targets or "up" in targets, "down": "down" in targets}
+    full = sum(v for k, v in per_layer.items() if has[k])
+    tail = (per_layer["qkv"] if has["qkv"] else 0) if kv_tail else full
+    return {"norm": norm, "lora_down": (h - 1) * full + tail}
 
 
 def main():
@@ -85,6 +126,8 @@ def main():
     ap.add_argument("--seed", type=int, default=7)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-tokens", type=int, default=8192)
+    ap.add_argument("--no-hidden-out", action="store_true",
+                    help="window without hidden_out: the last layer runs its K/V projections only")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: the recomputation path is built and measured on a single MI355X "
@@ -99,6 +142,7 @@ def main():
     crf.load()
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
+    device = crf.device_info(0)
     if args.workload == "drift":
         return bench_drift(args)
     if args.workload == "qwen15b_mixed8":
@@ -124,8 +168,10 @@ def main():
     kv = crf.kv_cache(case.k_pool, case.v_pool, case.block_table_dev, win.n_tokens, wl.page_size)
     stream = torch.cuda.current_stream()
 
+    hout = None if args.no_hidden_out else case.hidden_out
+
     def step():
-        crf.recompute_window(ctx, cd, case.hidden_dev, weights, lora, win.l0, win.h, kv, case.hidden_out, stream)
+        crf.recompute_window(ctx, cd, case.hidden_dev, weights, lora, win.l0, win.h, kv, hout, stream)
 
     for _ in range(args.warmup):
         step()
@@ -146,7 +192,12 @@ def main():
     ms = 1e3 * elapsed / args.steps
     tl_per_s = win.n_tokens * win.h * args.steps / elapsed
     f_win, f_parts = window_flops(dims, win.n_tokens, win.h, wl.lora_rank, wl.lora_targets)
+    if args.no_hidden_out:
+        f_win -= tail_skipped_flops(dims, win.n_tokens, wl.lora_rank, wl.lora_targets)
     kflops = kernel_flops(dims, win.n_tokens, wl.lora_rank, wl.lora_targets)
+    if args.no_hidden_out:
+        kflops.pop("gemm_qkv")   # the tail layer's launch is K/V-only: launches differ in size
+    hbm = hbm_bytes(dims, win.n_tokens, win.h, wl.lora_rank, wl.lora_targets, args.no_hidden_out)
     kernels = {}
     for k, (tot_ms, cnt) in timing.items():
         if cnt:
@@ -154,6 +205,8 @@ def main():
             e = {"avg_ms": round(avg, 4), "launches": cnt, "share": round(tot_ms / (ms * args.steps), 4)}
             if k in kflops:
                 e["tflops"] = round(kflops[k] / (avg * 1e-3) / 1e12, 1)
+            if k in hbm:
+                e["gbps"] = round(hbm[k] * args.steps / (tot_ms * 1e-3) / 1e9, 1)
             kernels[k] = e
     dom = max((k for k in kernels if k in kflops), key=lambda k: timing[k][0])
     dom_avg_s = timing[dom][0] / timing[dom][1] * 1e-3
@@ -181,9 +234,11 @@ def main():
         "data": "synthetic (seeded N(0,1) boundary state, random-init N(0,0.02) weights, LoRA A~N(0,1/8), "
                 "B~N(0,0.01)+N(0,0.005)); no dataset or checkpoint",
         "config": {
-            "workload": f"{wl.name}: Qwen2.5-7B-shaped bounded window, {win.n_tokens}-token prefix, layers "
+            "workload": f"{wl.name}: {SHAPE_NAME.get(dims.d_model, 'synthetic')}-shaped bounded window, "
+                        f"{win.n_tokens}-token prefix, layers "
                         f"[{win.l0},{win.l0 + win.h}) of {dims.n_layers}, LoRA rank {wl.lora_rank} on "
-                        f"{','.join(wl.lora_targets)}, paged KV {wl.page_size}-token pages",
+                        f"{','.join(wl.lora_targets)}, paged KV {wl.page_size}-token pages"
+                        + (", no hidden output (K/V-only last layer)" if args.no_hidden_out else ""),
             "n_tokens": win.n_tokens, "l0": win.l0, "h": win.h, "d_model": dims.d_model, "n_q_heads": dims.n_q_heads,
             "n_kv_heads": dims.n_kv_heads, "head_dim": dims.head_dim, "d_ffn": dims.d_ffn, "lora_rank": wl.lora_rank,
         },
@@ -193,15 +248,17 @@ def main():
                      "peak": PEAK_BF16 / 1e12, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16, 4),
                      "traffic": traffic},
         "kernels": kernels,
+        "device": device,
     }
     if not args.no_cpu_baseline:
         ns = min(args.cpu_sample_tokens, win.n_tokens)
         print(f"[bench] cpu baseline: oracle on {ns} tokens ...", file=sys.stderr, flush=True)
-        v, dt, thr = cpu_baseline(case, ns)
+        v, dt, thr, blas = cpu_baseline(case, ns)
         out["cpu_baseline"] = {
             "value": round(v, 1), "unit": "token-layers/s", "cores": thr, "kind": "oracle",
             "sample": f"fp64 numpy oracle, first {ns} of {win.n_tokens} prefix tokens through layers "
                       f"[{win.l0},{win.l0 + win.h}) ({dt:.1f} s; causal attention over that shorter prefix)",
+            "cpu": cpu_model(), "blas": blas,
         }
     print(json.dumps(out), flush=True)
 

@@ -165,7 +165,13 @@ crf_status crf_validate_window(const crf_model_dims *dims, int32_t l0, int32_t h
  *   base_weights: host array [n_layers]; only the window's entries are read.
  *   lora:         host array [n_layers] of the current adapter, or NULL (no adapter).
  *   hidden_out:   [n_tokens, d_model] receives H_{l0+h-1}; may be NULL; may alias
- *                 hidden_at_boundary.
+ *                 hidden_at_boundary.  When NULL, nothing reads the last
+ *                 window layer's output, and that layer's cache entry depends
+ *                 on its input only through the K and V projections
+ *                 (supplementary Eq. sup-layer-cache-dependency:
+ *                 C_l = G_l(H_{l-1})), so on the bf16 path it runs RMSNorm and
+ *                 the K/V projections (LoRA, bias, rotary, page write) only.
+ *                 The K/V written are the same either way.
  * h == 0 is direct reuse: nothing is launched and hidden_out (if given and
  * distinct) is not written.  Layers outside the window and pages outside the
  * block table are never touched.  n_tokens comes from kv_cache->n_tokens and
@@ -224,6 +230,13 @@ crf_status crf_context_device_errors(crf_context *ctx, int32_t *flags_out);
  * summed milliseconds and launch counts since the last read, then resets. */
 crf_status crf_context_set_timing(crf_context *ctx, int32_t enable);
 crf_status crf_context_read_timing(crf_context *ctx, float *ms_out, int32_t *count_out, int32_t n_kinds);
+
+/* Device facts for reporting measurements against the hardware's peak:
+ * compute-unit count, peak engine clock (MHz) and the architecture name
+ * (written NUL-terminated into name, at most name_len bytes; name may be NULL).
+ * Errors: INVALID_ARG (null outputs), HIP. */
+crf_status crf_device_info(int32_t device, int32_t *n_cu_out, int32_t *max_sclk_mhz_out, char *name,
+                           int32_t name_len);
 
 #ifdef __cplusplus
 }

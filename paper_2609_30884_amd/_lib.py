@@ -68,7 +68,8 @@ _LIB: Optional[ctypes.CDLL] = None
 
 EXPORTS = ("crf_status_string", "crf_abi_version", "crf_context_create", "crf_context_destroy", "crf_last_error",
            "crf_validate_dims", "crf_validate_window", "crf_recompute_window", "crf_recompute_window_batched",
-           "crf_layer_drift", "crf_context_device_errors", "crf_context_set_timing", "crf_context_read_timing")
+           "crf_layer_drift", "crf_context_device_errors", "crf_context_set_timing", "crf_context_read_timing",
+           "crf_device_info")
 
 
 def load(path: str = LIB_PATH) -> ctypes.CDLL:
@@ -107,6 +108,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.crf_context_set_timing.argtypes = [VP, I32]
     lib.crf_context_read_timing.restype = I32
     lib.crf_context_read_timing.argtypes = [VP, P(ctypes.c_float), P(I32), I32]
+    lib.crf_device_info.restype = I32
+    lib.crf_device_info.argtypes = [I32, P(I32), P(I32), ctypes.c_char_p, I32]
     _LIB = lib
     return lib
 
@@ -222,6 +225,15 @@ class Context:
         cnt = (ctypes.c_int32 * n)()
         _err(self.lib, self.handle, self.lib.crf_context_read_timing(self.handle, ms, cnt, n))
         return {k: (float(ms[i]), int(cnt[i])) for i, k in enumerate(KERNEL_KINDS)}
+
+
+def device_info(device: int = 0) -> Dict[str, object]:
+    """Compute-unit count, peak engine clock and architecture of a device."""
+    lib = load()
+    cu, mhz = ctypes.c_int32(), ctypes.c_int32()
+    name = ctypes.create_string_buffer(64)
+    _err(lib, None, lib.crf_device_info(device, ctypes.byref(cu), ctypes.byref(mhz), name, 64))
+    return {"arch": name.value.decode(), "compute_units": int(cu.value), "max_sclk_mhz": int(mhz.value)}
 
 
 def status_string(st: int) -> str:

@@ -284,6 +284,31 @@ crf_status run_layers_bf16(crf_context *ctx, const void *hb, const crf_layer_wei
     LAUNCH(ctx, s, CRF_KK_NORM,
            launch_rmsnorm(s, first ? hb : (const void *)ctx->hres, !first, w.attn_norm, false, xn, false,
                           first ? ctx->hres : nullptr, M, D, d.rms_eps));
+    if (last && !hout) {
+      // Nothing reads this layer's output: its cache entry depends only on its
+      // input through the K and V projections, so only those run.
+      const bool kv_any = lora_targets({CRF_K, CRF_V}, tg);
+      if (kv_any) LAUNCH(ctx, s, CRF_KK_LORA_DOWN, launch_lora_down_bf16(s, xn, D, M, D, tg, 2, rp, u, ldu));
+      GemmParams p = base_params(xn, D, 2 * dkv);
+      p.w[1] = (const bf16 *)w.w[CRF_K];
+      p.w[2] = (const bf16 *)w.w[CRF_V];
+      p.seg1 = 0;  // no query rows: [0, dkv) K, [dkv, 2 dkv) V
+      p.seg2 = dkv;
+      if (kv_any) {
+        p.U = u;
+        for (int i = 1; i < 3; ++i) {
+          const int t = CRF_Q + i;
+          p.lb[i] = has_lora(lora, l, t) ? (const bf16 *)lora[l].B[t] : nullptr;
+          p.ucol[i] = (i - 1) * rp;
+        }
+      }
+      p.bias[1] = (const bf16 *)w.bias_k;
+      p.bias[2] = (const bf16 *)w.bias_v;
+      p.dq = dq;
+      p.kv = layer_kv(ctx, kv, l);
+      LAUNCH(ctx, s, CRF_KK_GEMM_QKV, launch_gemm_bf16(s, EPI_QKV, hd, p));
+      break;
+    }
     bool any = lora_targets({CRF_Q, CRF_K, CRF_V}, tg);
     if (any) LAUNCH(ctx, s, CRF_KK_LORA_DOWN, launch_lora_down_bf16(s, xn, D, M, D, tg, 3, rp, u, ldu));
     {
@@ -677,3 +702,17 @@ crf_status crf_context_read_timing(crf_context *ctx, float *ms_out, int32_t *cou
 }
 
 }  // extern "C"
+
+crf_status crf_device_info(int32_t device, int32_t *n_cu_out, int32_t *max_sclk_mhz_out, char *name,
+                           int32_t name_len) {
+  if (!n_cu_out || !max_sclk_mhz_out) return fail(nullptr, CRF_ERR_INVALID_ARG, "null output");
+  hipDeviceProp_t prop;
+  const hipError_t e = hipGetDeviceProperties(&prop, device);
+  if (e != hipSuccess) return fail(nullptr, CRF_ERR_HIP, "hipGetDeviceProperties: %s", hipGetErrorString(e));
+  *n_cu_out = prop.multiProcessorCount;
+  *max_sclk_mhz_out = prop.clockRate / 1000;
+  if (name && name_len > 0) {
+    snprintf(name, (size_t)name_len, "%s", prop.gcnArchName);
+  }
+  return CRF_OK;
+}

@@ -26,14 +26,37 @@
 namespace crf {
 namespace {
 
-constexpr int BM = 256, BN = 256, BK = 64;
-constexpr int STAGES = 2;
-constexpr int GROUP_M = 8;
+#ifndef CRF_GEMM_BK
+#define CRF_GEMM_BK 64
+#endif
+#ifndef CRF_GEMM_STAGES
+#define CRF_GEMM_STAGES 2
+#endif
+#ifndef CRF_GEMM_WAVES
+#define CRF_GEMM_WAVES 8
+#endif
 
-// 128-byte rows (64 bf16), eight 16-byte chunks; chunk c of row r sits at
-// position c ^ ((r / 2) % 8): the 16 rows a ds_read_b128 quarter-wave touches
-// hit 16 distinct 4-bank groups.
-CRF_DEV int swz(int row, int chunk) { return row * BK + ((chunk ^ ((row >> 1) & 7)) << 3); }
+constexpr int BM = 256, BN = 256;
+constexpr int BK = CRF_GEMM_BK;          // k-width of one LDS slice
+constexpr int STAGES = CRF_GEMM_STAGES;  // slices resident in LDS (STAGES * 32 KB per 32 of BK)
+constexpr int GROUP_M = 8;
+constexpr int LPR = BK / 8;              // 16-byte chunks (lanes) per row of a slice
+constexpr int RPB = 64 / LPR;            // rows per 1 KB DMA block
+static_assert(BK == 32 || BK == 64, "slice width");
+static_assert(STAGES >= 2 && STAGES * (BM + BN) * BK * 2 <= 160 * 1024, "LDS budget");
+
+// Chunk c of slice row r sits at position c ^ s(r), s(r) = (r / 2) % 8 for
+// 128-byte rows and (r / 4) % 4 for 64-byte rows: the 16 rows one quarter of a
+// ds_read_b128 touches (same chunk) hit 16 distinct 16-byte bank groups.
+CRF_DEV int swz(int row, int chunk) {
+  if (BK == 64) return row * BK + ((chunk ^ ((row >> 1) & 7)) << 3);
+  return row * BK + ((chunk ^ ((row >> 2) & 3)) << 3);
+}
+
+template <int N>
+CRF_DEV void wait_vm() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
 
 template <int EPI>
 CRF_DEV const bf16 *weight_row(const GemmParams &p, int r) {
@@ -70,7 +93,7 @@ __global__ __launch_bounds__(64 * WAVES, 1) void gemm_bf16_kernel(const GemmPara
   constexpr int WM_COUNT = WAVES / 2;      // token groups
   constexpr int WTM = BM / WM_COUNT;       // tokens per wave: 128 or 64
   constexpr int NJ = WTM / 32;             // 32-token blocks per wave
-  constexpr int BLK = (BM / 8) / WAVES;    // 1 KB DMA blocks per operand per wave per slice
+  constexpr int BLK = (BM / RPB) / WAVES;  // 1 KB DMA blocks per operand per wave per slice
   constexpr int DMA_PER_SLICE = 2 * BLK;
   extern __shared__ __align__(16) bf16 smem[];
   bf16 *const lds_x = smem;                       // [STAGES][BM*BK]
@@ -91,24 +114,24 @@ __global__ __launch_bounds__(64 * WAVES, 1) void gemm_bf16_kernel(const GemmPara
   const int wn = wave / WM_COUNT, wm = wave % WM_COUNT;
   const int g = lane / 32, l32 = lane % 32;
 
-  // ---- global -> LDS DMA.  A slice of one operand is 256 rows x 64 k = 32 x 1 KB
-  // blocks; wave w moves blocks WAVES*j + w.  Inside a block, lane L writes LDS
-  // bytes [16 L, 16 L + 16): row 8*block + L/8, swizzled position L%8, which
-  // holds logical k-chunk (L%8) ^ ((row/2)%8) of that row.
+  // ---- global -> LDS DMA.  A slice of one operand is 256 rows x BK k = BK/2
+  // blocks of 1 KB; wave w moves blocks WAVES*j + w.  Inside a block, lane L
+  // writes LDS bytes [16 L, 16 L + 16): row RPB*block + L/LPR, swizzled
+  // position L%LPR, which holds the logical k-chunk at that position of swz.
   const __amdgpu_buffer_rsrc_t xres = make_rsrc(p.X, (uint32_t)((int64_t)p.M * p.ldx * 2));
   uint32_t xoff[BLK], woff[BLK];
   __amdgpu_buffer_rsrc_t wres[BLK];
 #pragma unroll
   for (int j = 0; j < BLK; ++j) {
     const int blk = WAVES * j + wave;
-    const int row = blk * 8 + lane / 8;
-    const int c = (lane % 8) ^ ((row >> 1) & 7);
+    const int row = blk * RPB + lane / LPR;
+    const int c = BK == 64 ? (lane % 8) ^ ((row >> 1) & 7) : (lane % 4) ^ ((row >> 2) & 3);
     const int xr = m0 + row;
     xoff[j] = xr < p.M ? (uint32_t)(((int64_t)xr * p.ldx + c * 8) * 2) : CRF_OOB;
-    // weight rows: the 8 rows of a block sit in one 64-row group, inside one segment
+    // weight rows: the RPB rows of a block sit in one 64-row group, inside one segment
     const int wr = n0 + row;
     int lr0, local;
-    const int sg = segment_of<EPI>(p, min(n0 + blk * 8, p.N - 1), lr0);
+    const int sg = segment_of<EPI>(p, min(n0 + blk * RPB, p.N - 1), lr0);
     const int seg_rows = EPI == EPI_QKV ? (sg == 0 ? p.seg1 : sg == 1 ? p.seg2 - p.seg1 : p.N - p.seg2)
                                         : (EPI == EPI_SWIGLU ? p.N / 2 : p.N);
     segment_of<EPI>(p, min(wr, p.N - 1), local);
@@ -182,38 +205,44 @@ __global__ __launch_bounds__(64 * WAVES, 1) void gemm_bf16_kernel(const GemmPara
       for (int j = 0; j < NJ; ++j) acc[i][j] = mfma32(fa[i], fb[j], acc[i][j]);
     __builtin_amdgcn_sched_barrier(0);
   };
-  // prologue: slices 0 and 1 in flight, slice 0 published, its step-0 fragments loaded
-  dma(0, 0);
-  if (nk > 1) {
-    dma(BK, 1);
-    if (DMA_PER_SLICE == 16)
-      asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
-    else
-      asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
-  } else {
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  }
+  // Ring of STAGES slices.  The prologue puts slices 0..STAGES-1 in flight.  At
+  // the end of slice kt (its last fragments already in registers): wait for
+  // slice kt+1 (own DMA; later slices may stay in flight), a bare barrier that
+  // publishes every wave's part and retires all reads of slice kt, refill that
+  // stage with slice kt+STAGES, read slice kt+1's first fragments, and run the
+  // last MFMA group of slice kt.  Fragment reads run one MFMA group ahead.
+  constexpr int KSTEPS = BK / 16;
+#pragma unroll
+  for (int s = 0; s < STAGES; ++s)
+    if (s < nk) dma(s * BK, s);
+  if (nk >= STAGES)
+    wait_vm<(STAGES - 1) * DMA_PER_SLICE>();
+  else
+    wait_vm<0>();
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
   bf16x8 a0[4], b0[NJ], a1[4], b1[NJ];
   frag(0, 0, a0, b0);
-  // Per slice kt: four k-steps of MFMAs with the next step's fragments read
-  // ahead; before the last step, wait for slice kt+1 (own DMA, then a bare
-  // barrier publishing every wave's part and retiring all reads of slice kt),
-  // refill this stage with slice kt+2 and read slice kt+1's first fragments.
+  int st = 0;
   for (int kt = 0; kt < nk; ++kt) {
-    const int st = kt & 1;
-    frag(st, 1, a1, b1);
-    mm(a0, b0);
-    frag(st, 2, a0, b0);
-    mm(a1, b1);
-    frag(st, 3, a1, b1);
-    mm(a0, b0);
-    if (kt + 1 < nk) {
-      asm volatile("s_waitcnt vmcnt(0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-      if (kt + 2 < nk) dma((kt + 2) * BK, st);
-      frag(st ^ 1, 0, a0, b0);
+#pragma unroll
+    for (int s = 0; s < KSTEPS; s += 2) {
+      // k-step s uses (a0, b0), k-step s+1 uses (a1, b1)
+      frag(st, s + 1, a1, b1);
+      mm(a0, b0);
+      if (s + 2 < KSTEPS) {
+        frag(st, s + 2, a0, b0);
+      } else if (kt + 1 < nk) {
+        if (kt + STAGES - 1 < nk)
+          wait_vm<(STAGES - 2) * DMA_PER_SLICE>();
+        else
+          wait_vm<0>();
+        asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+        if (kt + STAGES < nk) dma((kt + STAGES) * BK, st);
+        frag(st + 1 == STAGES ? 0 : st + 1, 0, a0, b0);
+      }
+      mm(a1, b1);
     }
-    mm(a1, b1);
+    st = st + 1 == STAGES ? 0 : st + 1;
   }
 
   // ---- epilogues
@@ -333,10 +362,6 @@ hipError_t go(hipStream_t s, const GemmParams &p) {
   hipLaunchKernelGGL((gemm_bf16_kernel<EPI, HD, WAVES>), dim3(tiles), dim3(64 * WAVES), lds, s, p);
   return hipGetLastError();
 }
-
-#ifndef CRF_GEMM_WAVES
-#define CRF_GEMM_WAVES 8
-#endif
 
 }  // namespace
 

@@ -140,6 +140,34 @@ def test_bf16_page_sizes_and_head_shapes(page_size, hd, nq, nkv, n):
     _untouched(case, set(kv))
 
 
+@pytest.mark.parametrize("name,n,l0,h,seed", [
+    ("qwen15b_4k", 1000, 10, 2, 7),
+    ("qwen15b_4k", 600, 5, 1, 17),     # a one-layer window is all tail
+    ("qwen7b_16k", 333, 14, 2, 29),
+])
+def test_bf16_kv_only_tail_layer(name, n, l0, h, seed):
+    """Without hidden_out the last window layer runs only its K/V projections
+    (its cache entry depends on its input alone, supplementary Eq.
+    sup-layer-cache-dependency): every page written is bitwise the full run's,
+    and within tolerance of the oracle."""
+    from synthetic.device import build_case, canary_fill
+    wl = syn.WORKLOADS[name].with_window(n_tokens=n, l0=l0, h=h)
+    case = build_case(wl, seed)
+    print(f"[case] kv-only tail {name} n={n} window=[{l0},{l0 + h}) seed={seed}", flush=True)
+    ctx = run_gpu_window(case)
+    torch.cuda.synchronize()
+    k_full, v_full, h_full = case.k_pool.clone(), case.v_pool.clone(), case.hidden_out.clone()
+    canary_fill(case.k_pool)
+    canary_fill(case.v_pool)
+    run_gpu_window(case, ctx=ctx, hidden_out=False)
+    torch.cuda.synchronize()
+    assert bits_equal(case.k_pool, k_full) and bits_equal(case.v_pool, v_full)
+    assert bits_equal(case.hidden_out, h_full)      # not written by the second call
+    out, kv = oracle_window(case)
+    assert_window_parity(case, out, kv, label=f"kv-only tail {name} n={n}")
+    _untouched(case, set(kv))
+
+
 def test_bf16_qkv_bias_and_rank8():
     """Optional q/k/v biases and a rank-8 adapter on the bf16 path."""
     from synthetic.device import build_case
