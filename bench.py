@@ -10,8 +10,9 @@ pages), inputs resident in HBM before the timed region.  Prints one JSON line.
 Other workloads (one JSON line each): tiny_f32, qwen15b_4k, qwen7b_16k_suffix
 (the 24-layer affected suffix), qwen15b_mixed8 (8 ragged stale caches through
 the batched call), drift (crf_layer_drift over 28 layers and 4 stored
-adapter versions at 1.5B shapes) and copy (a 1 GiB elementwise pass that
-calibrates the HBM byte counters).
+adapter versions at 1.5B shapes), trajectory (maintenance over 32 adapter
+updates: fresh, exact suffix, drift policy, reuse) and copy (a 1 GiB
+elementwise pass that calibrates the HBM byte counters).
 """
 from __future__ import annotations
 
@@ -126,6 +127,7 @@ def main():
     ap.add_argument("--seed", type=int, default=7)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-tokens", type=int, default=8192)
+    ap.add_argument("--updates", type=int, default=32, help="trajectory workload: number of adapter updates")
     ap.add_argument("--no-hidden-out", action="store_true",
                     help="window without hidden_out: the last layer runs its K/V projections only")
     args = ap.parse_args()
@@ -149,6 +151,8 @@ def main():
         return bench_mixed(args)
     if args.workload == "copy":
         return bench_copy(args)
+    if args.workload == "trajectory":
+        return bench_trajectory(args)
     wl = syn.WORKLOADS[args.workload]
     dims = wl.dims
     win = wl.window
@@ -366,6 +370,61 @@ def bench_drift(args):
                      "traffic": None},
         "kernels": {k: {"avg_ms": round(v[0] / v[1], 4), "launches": v[1]} for k, v in timing.items() if v[1]},
     }
+    print(json.dumps(out), flush=True)
+
+
+def bench_trajectory(args):
+    """Maintenance over a sequence of adapter updates on the 7B/16K shapes
+    (host recovery loop): fresh full recomputation, exact suffix, the drift
+    policy and reuse, each on its own copy of the prefix."""
+    import torch
+    import paper_2609_30884_amd as crf
+    import synthetic as syn
+    from paper_2609_30884_amd.recovery import AdapterVersions, CacheState, Executor, RecoveryLoop, Update
+    from synthetic.trajectory import make_setup, make_state_buffers, new_b
+    wl = syn.WORKLOADS["qwen7b_16k"]
+    dims, n = wl.dims, wl.window.n_tokens
+    t0 = time.perf_counter()
+    setup = make_setup(wl, args.seed, n, args.updates)
+    cd = crf.make_dims(dims.n_layers, dims.d_model, dims.n_q_heads, dims.n_kv_heads, dims.head_dim, dims.d_ffn,
+                       dims.rms_eps, dims.rope_theta, dims.dtype)
+    ctx = crf.Context(cd, n, wl.lora_rank)
+    weights = crf.layer_weights_array(setup.weights)
+    adapters = AdapterVersions(setup.base_lora)
+    keep, states = [], {}
+    for name in ("fresh", "suffix", "policy"):
+        k, v, bnd = make_state_buffers(setup, wl.page_size)
+        keep.append((k, v, bnd))
+        states[name] = CacheState(crf.kv_cache(k, v, setup.block_table, n, wl.page_size), bnd)
+    stream = torch.cuda.current_stream()
+    ex = Executor(ctx, cd, weights, stream)
+    for st in states.values():   # every copy starts as a fresh prefill under version 0
+        ex.recompute(st, adapters.array(0), 0, dims.n_layers)
+    torch.cuda.synchronize()
+    print(f"[bench] trajectory set-up and prefills in {time.perf_counter() - t0:.1f}s", file=sys.stderr, flush=True)
+    drift = torch.empty(dims.n_layers, device="cuda")
+    risk = torch.empty_like(drift)
+    loop = RecoveryLoop(ex, adapters, dict(states, reuse=None), dims.n_layers, setup.sensitivity, drift, risk)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(args.seed + 1)
+    for i, (layer, target) in enumerate(setup.updates):
+        ver = adapters.apply(layer, target, new_b(setup, adapters.versions[-1], layer, target, g))
+        recs = loop.step(Update(ver, layer, target))
+        pol = next(r for r in recs if r.strategy == "policy")
+        print(f"[bench] update {i + 1}/{len(setup.updates)}: {target}@{layer} policy {pol.decision.action} "
+              f"[{pol.r},{pol.b}) " + " ".join(f"{r.strategy}={1e3 * r.seconds:.1f}ms" for r in recs),
+              file=sys.stderr, flush=True)
+    assert ctx.device_errors() == 0
+    summ = loop.summary()
+    out = {"metric": "maintenance ms over an update trajectory (7B-shape, 16K-token prefix); lower is better",
+           "value": summ["policy"]["maintenance_ms"], "unit": "ms", "n_gpus": 1, "steps": len(setup.updates),
+           "warmup": 0, "ms_per_step": round(summ["policy"]["maintenance_ms"] / len(setup.updates), 3),
+           "higher_is_better": False, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+           "data": "synthetic (seeded device draws; one B factor moves by N(0,0.005) per update)",
+           "config": {"workload": f"trajectory: {len(setup.updates)} updates, Qwen2.5-7B shapes, {n}-token prefix, "
+                                  f"{dims.n_layers} layers, LoRA rank {wl.lora_rank} on {','.join(wl.lora_targets)}",
+                      "updates": [f"{t}@{l}" for l, t in setup.updates]},
+           "strategies": summ}
     print(json.dumps(out), flush=True)
 
 

@@ -1,0 +1,85 @@
+"""Seeded synthetic set-up for an update trajectory (device placement only).
+
+A whole model (every layer's weights), a base LoRA adapter, the embedding
+state H_{-1}, maintained cache states (paged K/V pools and one retained
+boundary state per layer) and a sequence of single-factor adapter updates.
+Values are drawn on the device from a seeded torch generator (weights
+N(0, 0.02), RMSNorm gains 1 + N(0, 0.02), A ~ N(0, 1/8), B ~ N(0, 0.01), each
+update adds N(0, 0.005) to one B factor), so a 28-layer 7B-shaped model is
+ready in seconds.  Computes no part of the method.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+from typing import Dict, List
+
+import numpy as np
+import torch
+
+from . import TARGETS, Dims, Workload, gen_block_table
+from .device import canary_fill
+
+
+def _randn(g: torch.Generator, shape, std: float, mean: float = 0.0) -> torch.Tensor:
+    x = torch.randn(shape, generator=g, device="cuda", dtype=torch.float32)
+    return (x * std + mean).to(torch.bfloat16).contiguous()
+
+
+@dataclass
+class TrajectorySetup:
+    dims: Dims
+    n_tokens: int
+    weights: List[Dict[str, torch.Tensor]]
+    base_lora: List[dict]
+    embedding: torch.Tensor
+    block_table: torch.Tensor
+    n_phys: int
+    updates: List[tuple]           # (layer, target) per update
+    sensitivity: torch.Tensor      # [n_layers] fp32
+
+
+def make_setup(wl: Workload, seed: int, n_tokens: int, n_updates: int) -> TrajectorySetup:
+    d: Dims = wl.dims
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed)
+    weights, lora = [], []
+    for l in range(d.n_layers):
+        w = {"attn_norm": _randn(g, (d.d_model,), 0.02, 1.0), "mlp_norm": _randn(g, (d.d_model,), 0.02, 1.0)}
+        ll = {"rank": wl.lora_rank, "scale": wl.lora_scale, "targets": {}}
+        for t in TARGETS:
+            d_out, d_in = d.target_shape(t)
+            w["w_" + t] = _randn(g, (d_out, d_in), 0.02)
+            if t in wl.lora_targets:
+                ll["targets"][t] = (_randn(g, (wl.lora_rank, d_in), 1 / 8), _randn(g, (d_out, wl.lora_rank), 0.01))
+        weights.append(w)
+        lora.append(ll)
+    emb = torch.randn((n_tokens, d.d_model), generator=g, device="cuda").to(torch.bfloat16)
+    bt, n_phys = gen_block_table(wl, seed, n_tokens)
+    rng = np.random.default_rng(np.random.SeedSequence(seed, spawn_key=(wl.config_id, 991)))
+    updates = [(int(rng.integers(d.n_layers)), str(rng.choice(list(wl.lora_targets)))) for _ in range(n_updates)]
+    # sensitivity: s_l = u_l * exp(-l / 6) / E[d], u_l ~ U(0.5, 1.5), E[d] the mean norm of one update's
+    # change; early layers trigger after one or two updates, deep layers only once drift has accumulated
+    step_norm = np.mean([0.005 * np.sqrt(np.prod(d.target_shape(t)[:1]) * wl.lora_rank) for t in wl.lora_targets])
+    u = rng.uniform(0.5, 1.5, d.n_layers)
+    s = (u * np.exp(-np.arange(d.n_layers) / 6.0) / step_norm).astype(np.float32)
+    return TrajectorySetup(d, n_tokens, weights, lora, emb, torch.from_numpy(bt).cuda(), n_phys, updates,
+                           torch.from_numpy(s).cuda())
+
+
+def new_b(setup: TrajectorySetup, lora_now: List[dict], layer: int, target: str, g: torch.Generator) -> torch.Tensor:
+    """The updated B factor: the current one plus N(0, 0.005)."""
+    b = lora_now[layer]["targets"][target][1]
+    return (b.float() + 0.005 * torch.randn(b.shape, generator=g, device="cuda")).to(torch.bfloat16).contiguous()
+
+
+def make_state_buffers(setup: TrajectorySetup, page_size: int):
+    """Paged K/V pools (canary-filled) and one boundary-state buffer per layer
+    boundary (boundaries[0] holds H_{-1})."""
+    d = setup.dims
+    shape = (d.n_layers, setup.n_phys, d.n_kv_heads, page_size, d.head_dim)
+    k = torch.empty(shape, dtype=torch.bfloat16, device="cuda")
+    v = torch.empty(shape, dtype=torch.bfloat16, device="cuda")
+    canary_fill(k)
+    canary_fill(v)
+    bnd = [setup.embedding] + [torch.empty_like(setup.embedding) for _ in range(d.n_layers)]
+    return k, v, bnd
