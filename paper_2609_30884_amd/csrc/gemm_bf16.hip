@@ -21,6 +21,8 @@
 // token, which makes every epilogue lane-local (a rotary pair (f, f+hd/2) and a
 // gate/up pair live in the same lane).  16-byte LDS chunks are XOR-swizzled by
 // (row/2) mod 8 so the fragment reads are bank-conflict free.
+#include <type_traits>
+
 #include "kernels.hpp"
 
 namespace crf {
@@ -198,52 +200,66 @@ __global__ __launch_bounds__(64 * WAVES, 1) void gemm_bf16_kernel(const GemmPara
     for (int j = 0; j < NJ; ++j) fb[j] = as_bf16x8(ld16(sx + swz(wm * WTM + 32 * j + l32, 2 * s + g)));
   };
   auto mm = [&](bf16x8 (&fa)[4], bf16x8 (&fb)[NJ]) {
-    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int j = 0; j < NJ; ++j) acc[i][j] = mfma32(fa[i], fb[j], acc[i][j]);
-    __builtin_amdgcn_sched_barrier(0);
   };
-  // Ring of STAGES slices.  The prologue puts slices 0..STAGES-1 in flight.  At
-  // the end of slice kt (its last fragments already in registers): wait for
-  // slice kt+1 (own DMA; later slices may stay in flight), a bare barrier that
-  // publishes every wave's part and retires all reads of slice kt, refill that
-  // stage with slice kt+STAGES, read slice kt+1's first fragments, and run the
-  // last MFMA group of slice kt.  Fragment reads run one MFMA group ahead.
+  // Ring of STAGES slices.  The prologue puts slices 0..STAGES-1 in flight.
+  // Each k-step is one scheduling region: its MFMAs with the next step's
+  // fragment reads interleaved one by one (the MFMAs use fragments read one
+  // region earlier).  The last k-step of a slice follows the slice's single
+  // barrier: wait for slice kt+1 (own DMA; later slices may stay in flight),
+  // a bare barrier that publishes every wave's part and retires all reads of
+  // slice kt, then the refill of that stage with slice kt+STAGES (clamped to
+  // the last slice near the end, so every slice issues the same number of
+  // loads), interleaved with the MFMAs and with slice kt+1's first reads.
   constexpr int KSTEPS = BK / 16;
+  constexpr int NMM = 4 * NJ, NDS = 4 + NJ;
+  auto interleave = [&](auto n_vmem) {
+    constexpr int NV = decltype(n_vmem)::value;
 #pragma unroll
-  for (int s = 0; s < STAGES; ++s)
-    if (s < nk) dma(s * BK, s);
-  if (nk >= STAGES)
-    wait_vm<(STAGES - 1) * DMA_PER_SLICE>();
-  else
-    wait_vm<0>();
+    for (int i = 0; i < NMM; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+      if (i < NV) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // one global load
+      if (i < NDS) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
+    }
+  };
+#pragma unroll
+  for (int s = 0; s < STAGES; ++s) dma(min(s, nk - 1) * BK, s);
+  wait_vm<(STAGES - 1) * DMA_PER_SLICE>();
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
   bf16x8 a0[4], b0[NJ], a1[4], b1[NJ];
   frag(0, 0, a0, b0);
   int st = 0;
   for (int kt = 0; kt < nk; ++kt) {
+    const int nst = st + 1 == STAGES ? 0 : st + 1;
 #pragma unroll
-    for (int s = 0; s < KSTEPS; s += 2) {
-      // k-step s uses (a0, b0), k-step s+1 uses (a1, b1)
-      frag(st, s + 1, a1, b1);
-      mm(a0, b0);
-      if (s + 2 < KSTEPS) {
-        frag(st, s + 2, a0, b0);
-      } else if (kt + 1 < nk) {
-        if (kt + STAGES - 1 < nk)
-          wait_vm<(STAGES - 2) * DMA_PER_SLICE>();
-        else
-          wait_vm<0>();
-        asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-        if (kt + STAGES < nk) dma((kt + STAGES) * BK, st);
-        frag(st + 1 == STAGES ? 0 : st + 1, 0, a0, b0);
+    for (int s = 0; s + 1 < KSTEPS; ++s) {
+      __builtin_amdgcn_sched_barrier(0);
+      if (s & 1) {
+        frag(st, s + 1, a0, b0);
+        mm(a1, b1);
+      } else {
+        frag(st, s + 1, a1, b1);
+        mm(a0, b0);
       }
-      mm(a1, b1);
+      interleave(std::integral_constant<int, 0>());
+      __builtin_amdgcn_sched_barrier(0);
     }
-    st = st + 1 == STAGES ? 0 : st + 1;
+    // also after the last slice (stage nst then holds a clamped copy): the loop
+    // body stays one basic block per region
+    wait_vm<(STAGES - 2) * DMA_PER_SLICE>();
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    __builtin_amdgcn_sched_barrier(0);
+    dma(min(kt + STAGES, nk - 1) * BK, st);
+    frag(nst, 0, a0, b0);
+    mm(a1, b1);  // KSTEPS is even: the last k-step of a slice uses (a1, b1)
+    interleave(std::integral_constant<int, DMA_PER_SLICE>());
+    __builtin_amdgcn_sched_barrier(0);
+    st = nst;
   }
+  wait_vm<0>();  // the clamped refills of the last slices
 
   // ---- epilogues
   if (EPI == EPI_RESID) {
