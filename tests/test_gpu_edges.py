@@ -1,0 +1,92 @@
+"""Degenerate and boundary cases of the bf16 path against the oracle:
+prefix lengths around the 16-token page, the 64-key attention tile, the
+128-query attention block and the 256-row GEMM tile (including n = 1, where
+attention returns V[0]); an empty prefix; no adapter and a partial adapter;
+and a prefix longer than the context's workspace."""
+import dataclasses
+
+import pytest
+
+import synthetic as syn
+from tests.helpers import assert_window_parity, bits_equal, cdims, oracle_window, run_gpu_window
+
+pytestmark = pytest.mark.gpu
+torch = pytest.importorskip("torch")
+
+SMALL = dict(n_layers=4, d_model=768, n_q_heads=12, n_kv_heads=2, head_dim=64, d_ffn=2048)
+
+
+def _wl(kind, n, **kw):
+    base = syn.WORKLOADS["qwen15b_4k"]
+    if kind == "small":
+        base = base.with_dims(**SMALL)
+    wl = base.with_window(n_tokens=n, l0=1, h=2)
+    return dataclasses.replace(wl, **kw) if kw else wl
+
+
+@pytest.mark.parametrize("kind,n", [("small", n) for n in (1, 2, 15, 16, 17, 63, 64, 65, 127, 128, 129, 255, 256, 257)]
+                         + [("qwen15b", n) for n in (1, 17, 129, 257)])
+def test_bf16_boundary_lengths(kind, n):
+    from synthetic.device import build_case
+    print(f"[case] {kind} n={n}", flush=True)
+    case = build_case(_wl(kind, n), 17)
+    run_gpu_window(case)
+    torch.cuda.synchronize()
+    out, kv = oracle_window(case)
+    assert_window_parity(case, out, kv, label=f"{kind} n={n}")
+
+
+@pytest.mark.parametrize("targets", [(), ("q", "v"), syn.TARGETS])
+def test_bf16_absent_and_partial_adapter(targets):
+    from synthetic.device import build_case
+    wl = _wl("small", 300, lora_targets=tuple(targets))
+    print(f"[case] adapter targets {targets}", flush=True)
+    case = build_case(wl, 29)
+    run_gpu_window(case)
+    torch.cuda.synchronize()
+    out, kv = oracle_window(case)
+    assert_window_parity(case, out, kv, label=f"targets={targets}")
+
+
+def test_bf16_null_adapter_equals_empty_adapter():
+    import paper_2609_30884_amd as crf
+    from synthetic.device import build_case
+    wl = _wl("small", 200, lora_targets=())
+    case = build_case(wl, 7)
+    ctx = run_gpu_window(case)
+    torch.cuda.synchronize()
+    k1, v1, h1 = case.k_pool.clone(), case.v_pool.clone(), case.hidden_out.clone()
+    kv = crf.kv_cache(case.k_pool, case.v_pool, case.block_table_dev, 200, wl.page_size)
+    crf.recompute_window(ctx, cdims(wl.dims), case.hidden_dev, crf.layer_weights_array(case.weights_dev), None,
+                         1, 2, kv, case.hidden_out)
+    torch.cuda.synchronize()
+    assert bits_equal(case.k_pool, k1) and bits_equal(case.v_pool, v1) and bits_equal(case.hidden_out, h1)
+
+
+def test_bf16_empty_prefix_is_noop():
+    import paper_2609_30884_amd as crf
+    from synthetic.device import build_case, canary_mask
+    wl = _wl("small", 64)
+    case = build_case(wl, 7)
+    ctx = crf.Context(cdims(wl.dims), 64, wl.lora_rank)
+    kv = crf.kv_cache(case.k_pool, case.v_pool, case.block_table_dev, 0, wl.page_size)
+    case.hidden_out.zero_()
+    crf.recompute_window(ctx, cdims(wl.dims), case.hidden_dev, crf.layer_weights_array(case.weights_dev),
+                         crf.lora_array(case.lora_dev, wl.dims.n_layers), 1, 2, kv, case.hidden_out)
+    torch.cuda.synchronize()
+    assert bool(canary_mask(case.k_pool).all()) and bool(canary_mask(case.v_pool).all())
+    assert bool((case.hidden_out == 0).all())
+    assert ctx.device_errors() == 0
+
+
+def test_prefix_longer_than_workspace_is_rejected():
+    import paper_2609_30884_amd as crf
+    from synthetic.device import build_case, canary_mask
+    wl = _wl("small", 200)
+    case = build_case(wl, 7)
+    ctx = crf.Context(cdims(wl.dims), 100, wl.lora_rank)
+    with pytest.raises(crf.CrfError) as ei:
+        run_gpu_window(case, ctx=ctx)
+    assert ei.value.status == 5
+    torch.cuda.synchronize()
+    assert bool(canary_mask(case.k_pool).all()), "nothing may run when the request is rejected"
