@@ -90,3 +90,20 @@ def test_prefix_longer_than_workspace_is_rejected():
     assert ei.value.status == 5
     torch.cuda.synchronize()
     assert bool(canary_mask(case.k_pool).all()), "nothing may run when the request is rejected"
+
+
+@pytest.mark.parametrize("dims,n", [
+    (dict(n_layers=4, d_model=768, n_q_heads=12, n_kv_heads=2, head_dim=64, d_ffn=2048), 5500),
+    (dict(n_layers=4, d_model=768, n_q_heads=24, n_kv_heads=4, head_dim=128, d_ffn=1024), 2800),
+])
+def test_bf16_longer_prefixes(dims, n):
+    """Longer ragged prefixes (dozens of query blocks per head, more query
+    heads than model width) with head_dim 64 and 128."""
+    from synthetic.device import build_case
+    wl = syn.WORKLOADS["qwen15b_4k"].with_dims(**dims).with_window(n_tokens=n, l0=1, h=2)
+    print(f"[case] longer prefix {dims} n={n}", flush=True)
+    case = build_case(wl, 29)
+    run_gpu_window(case)
+    torch.cuda.synchronize()
+    out, kv = oracle_window(case)
+    assert_window_parity(case, out, kv, label=f"longer prefix n={n}")
