@@ -380,8 +380,9 @@ def bench_trajectory(args):
     import torch
     import paper_2609_30884_amd as crf
     import synthetic as syn
+    from paper_2609_30884_amd.policy import CalibrationCondition, layer_sensitivity
     from paper_2609_30884_amd.recovery import AdapterVersions, CacheState, Executor, RecoveryLoop, Update
-    from synthetic.trajectory import make_setup, make_state_buffers, new_b
+    from synthetic.trajectory import make_calibration_conditions, make_setup, make_state_buffers, new_b
     wl = syn.WORKLOADS["qwen7b_16k"]
     dims, n = wl.dims, wl.window.n_tokens
     t0 = time.perf_counter()
@@ -404,7 +405,9 @@ def bench_trajectory(args):
     print(f"[bench] trajectory set-up and prefills in {time.perf_counter() - t0:.1f}s", file=sys.stderr, flush=True)
     drift = torch.empty(dims.n_layers, device="cuda")
     risk = torch.empty_like(drift)
-    loop = RecoveryLoop(ex, adapters, dict(states, reuse=None), dims.n_layers, setup.sensitivity, drift, risk)
+    conds = [CalibrationCondition(*c) for c in make_calibration_conditions(wl, args.seed)]
+    sens = torch.from_numpy(layer_sensitivity(conds, dims.n_layers).astype("float32")).cuda()
+    loop = RecoveryLoop(ex, adapters, dict(states, reuse=None), dims.n_layers, sens, drift, risk)
     g = torch.Generator(device="cuda")
     g.manual_seed(args.seed + 1)
     for i, (layer, target) in enumerate(setup.updates):
@@ -424,7 +427,8 @@ def bench_trajectory(args):
            "config": {"workload": f"trajectory: {len(setup.updates)} updates, Qwen2.5-7B shapes, {n}-token prefix, "
                                   f"{dims.n_layers} layers, LoRA rank {wl.lora_rank} on {','.join(wl.lora_targets)}",
                       "updates": [f"{t}@{l}" for l, t in setup.updates]},
-           "strategies": summ}
+           "strategies": summ,
+           "sensitivity": [round(float(x), 4) for x in sens.cpu()]}
     print(json.dumps(out), flush=True)
 
 

@@ -17,11 +17,19 @@ The earliest cache layer an update can change depends on the module
 (supplementary Eq. sup-first-invalid-cache-layer): s for K/V updates,
 min(s+1, N) for Q/O/MLP updates (N = no cached layer invalidated); the
 executable restart is s whenever a later layer can be affected.
+
+The sensitivities s_l come from offline calibration (Sec. 4.1 "Offline
+calibration", Eqs. layer-recovery-label and layer-sensitivity): each
+calibration condition i (restart r_i, adapter distance d_i) evaluates the
+candidate windows H_i; the first safe one h*_i labels the layers it covers;
+per layer, delta_l is the order statistic of the covering conditions'
+distances just past a 5% lower tail, and s_l = 1 / delta_l (0 for a layer no
+selected window covers).
 """
 from __future__ import annotations
 
 from dataclasses import dataclass, field
-from typing import List, Optional, Sequence, Tuple
+from typing import Iterable, List, Mapping, Optional, Sequence, Tuple
 
 import numpy as np
 
@@ -92,3 +100,59 @@ class MixedVersionCache:
 
     def stale_layers(self, version: int) -> List[int]:
         return [int(l) for l in np.nonzero(self.anchor != version)[0]]
+
+
+# ----------------------------------------------------------------------------- offline calibration
+
+CANDIDATE_H = (0, 1, 2, 4, 8, 16)
+SAFE_KL, SAFE_TOP1, SAFE_SCORE_DROP = 0.05, 0.99, 0.01
+DELTA_TAIL, DELTA_FLOOR = 0.05, 1e-12
+
+
+def candidate_windows(r: int, n_layers: int) -> List[int]:
+    """H_i = {min(h, N - r) : h in {0, 1, 2, 4, 8, 16}} U {N - r}, ascending."""
+    rest = n_layers - r
+    return sorted({min(h, rest) for h in CANDIDATE_H} | {rest})
+
+
+def is_safe(kl: float, top1_agreement: float, score_drop: float) -> bool:
+    """A candidate is safe against fresh recomputation when first-step
+    next-token KL <= 0.05, top-1 agreement >= 0.99 and the full-answer task
+    score drops by at most 0.01."""
+    return kl <= SAFE_KL and top1_agreement >= SAFE_TOP1 and score_drop <= SAFE_SCORE_DROP
+
+
+def first_safe_window(safe: Mapping[int, bool]) -> Optional[int]:
+    """h* = min{h in H : S(h) = 1} (larger windows need not stay safe); None if none is."""
+    ok = [h for h, v in safe.items() if v]
+    return min(ok) if ok else None
+
+
+@dataclass(frozen=True)
+class CalibrationCondition:
+    r: int                 # restart layer
+    d: float               # l2 distance between the active adapter and the stale cache's adapter state
+    h_star: Optional[int]  # first safe window (None: no evaluated window was safe)
+
+
+def recovery_labels(cond: CalibrationCondition, n_layers: int) -> np.ndarray:
+    """y_{i,l} = 1[r_i <= l < r_i + h*_i]."""
+    y = np.zeros(n_layers, dtype=bool)
+    if cond.h_star:
+        y[cond.r:cond.r + cond.h_star] = True
+    return y
+
+
+def layer_sensitivity(conditions: Iterable[CalibrationCondition], n_layers: int) -> np.ndarray:
+    """s_l = 1 / delta_l with delta_l = max(d_{l,(floor(0.05 n_l) + 1)}, 1e-12), the
+    (1-based) order statistic of D_l^+ = {d_i : y_{i,l} = 1}; s_l = 0 when D_l^+ is empty."""
+    conds = list(conditions)
+    s = np.zeros(n_layers, dtype=np.float64)
+    for l in range(n_layers):
+        dl = np.sort([c.d for c in conds if recovery_labels(c, n_layers)[l]])
+        n = len(dl)
+        if n == 0:
+            continue
+        delta = max(float(dl[int(np.floor(DELTA_TAIL * n))]), DELTA_FLOOR)
+        s[l] = 1.0 / delta
+    return s

@@ -35,7 +35,6 @@ class TrajectorySetup:
     block_table: torch.Tensor
     n_phys: int
     updates: List[tuple]           # (layer, target) per update
-    sensitivity: torch.Tensor      # [n_layers] fp32
 
 
 def make_setup(wl: Workload, seed: int, n_tokens: int, n_updates: int) -> TrajectorySetup:
@@ -57,13 +56,36 @@ def make_setup(wl: Workload, seed: int, n_tokens: int, n_updates: int) -> Trajec
     bt, n_phys = gen_block_table(wl, seed, n_tokens)
     rng = np.random.default_rng(np.random.SeedSequence(seed, spawn_key=(wl.config_id, 991)))
     updates = [(int(rng.integers(d.n_layers)), str(rng.choice(list(wl.lora_targets)))) for _ in range(n_updates)]
-    # sensitivity: s_l = u_l * exp(-l / 6) / E[d], u_l ~ U(0.5, 1.5), E[d] the mean norm of one update's
-    # change; early layers trigger after one or two updates, deep layers only once drift has accumulated
-    step_norm = np.mean([0.005 * np.sqrt(np.prod(d.target_shape(t)[:1]) * wl.lora_rank) for t in wl.lora_targets])
-    u = rng.uniform(0.5, 1.5, d.n_layers)
-    s = (u * np.exp(-np.arange(d.n_layers) / 6.0) / step_norm).astype(np.float32)
-    return TrajectorySetup(d, n_tokens, weights, lora, emb, torch.from_numpy(bt).cuda(), n_phys, updates,
-                           torch.from_numpy(s).cuda())
+    return TrajectorySetup(d, n_tokens, weights, lora, emb, torch.from_numpy(bt).cuda(), n_phys, updates)
+
+
+def update_step_norm(wl: Workload) -> float:
+    """Mean l2 norm of one update's change (N(0, 0.005) on one B factor)."""
+    d = wl.dims
+    return float(np.mean([0.005 * np.sqrt(d.target_shape(t)[0] * wl.lora_rank) for t in wl.lora_targets]))
+
+
+def make_calibration_conditions(wl: Workload, seed: int, n: int = 256) -> List[tuple]:
+    """Synthetic calibration tuples (r_i, d_i, h*_i) standing in for the paper's
+    calibration split, which needs trained adapters and task data.  d_i is the
+    distance after k ~ U{1..8} accumulated updates (times a log-normal factor);
+    the window a condition needs grows with d_i and shrinks with depth,
+    h_need = floor(3 * d_i / E[d] * exp(-r_i / 8)) (0: reuse is safe), and h*_i
+    is the first candidate window {0, 1, 2, 4, 8, 16, N - r_i} (each capped at
+    N - r_i) at least that long."""
+    N = wl.dims.n_layers
+    e_d = update_step_norm(wl)
+    rng = np.random.default_rng(np.random.SeedSequence(seed, spawn_key=(wl.config_id, 992)))
+    out = []
+    for _ in range(n):
+        r = int(rng.integers(N))
+        k = int(rng.integers(1, 9))
+        dist = e_d * np.sqrt(k) * float(np.exp(rng.normal(0.0, 0.3)))
+        need = int(np.floor(3.0 * dist / e_d * np.exp(-r / 8.0)))
+        cands = sorted({min(h, N - r) for h in (0, 1, 2, 4, 8, 16)} | {N - r})
+        h_star = next((h for h in cands if h >= need), N - r)
+        out.append((r, dist, h_star))
+    return out
 
 
 def new_b(setup: TrajectorySetup, lora_now: List[dict], layer: int, target: str, g: torch.Generator) -> torch.Tensor:

@@ -18,8 +18,9 @@ torch = pytest.importorskip("torch")
 
 def test_recovery_trajectory_small():
     import paper_2609_30884_amd as crf
+    from paper_2609_30884_amd.policy import CalibrationCondition, layer_sensitivity
     from paper_2609_30884_amd.recovery import AdapterVersions, CacheState, Executor, RecoveryLoop, Update
-    from synthetic.trajectory import make_setup, make_state_buffers, new_b
+    from synthetic.trajectory import make_calibration_conditions, make_setup, make_state_buffers, new_b
     wl = dataclasses.replace(syn.WORKLOADS["qwen15b_4k"], lora_targets=syn.TARGETS).with_dims(
         n_layers=6, d_model=256, n_q_heads=2, n_kv_heads=1, head_dim=128, d_ffn=512)
     n, n_upd = 200, 8
@@ -42,7 +43,9 @@ def test_recovery_trajectory_small():
     assert bits_equal(bufs["suffix"][0], bufs["fresh"][0])
     drift = torch.empty(N, device="cuda")
     risk = torch.empty(N, device="cuda")
-    loop = RecoveryLoop(ex, adapters, dict(states, reuse=None), N, setup.sensitivity, drift, risk)
+    conds = [CalibrationCondition(*c) for c in make_calibration_conditions(wl, 7)]
+    sens = torch.from_numpy(layer_sensitivity(conds, N).astype(np.float32)).cuda()
+    loop = RecoveryLoop(ex, adapters, dict(states, reuse=None), N, sens, drift, risk)
     g = torch.Generator(device="cuda")
     g.manual_seed(123)
     for layer, target in setup.updates:
