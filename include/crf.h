@@ -200,6 +200,28 @@ crf_status crf_recompute_window_batched(crf_context *ctx, const crf_model_dims *
                                         const crf_layer_weights *base_weights, int32_t n_items,
                                         const crf_window_item *items, void *stream);
 
+/* First decoding step over a cached prefix (Sec. 3.2 "Tail Influence": the
+ * first-step next-token logits z, fresh or with a hybrid cache): the embedding
+ * states of n_new tokens [n_new, d_model] run through every layer 0..N-1 under
+ * `lora`, at positions kv_cache->n_tokens .. kv_cache->n_tokens + n_new - 1.
+ * At each layer they attend to that layer's cached K/V of the prefix (whatever
+ * adapter version produced each layer: a hybrid cache is just a pool whose
+ * layers come from different versions) and causally to each other; their own
+ * rotated K and V are written into the slots after the prefix.  Then the final
+ * RMSNorm (final_norm [d_model]) and the LM head (lm_head [vocab, d_model],
+ * nn.Linear layout) give the logits of the last new token:
+ * logits_out[vocab] (fp32, device).  The block table must cover
+ * kv_cache->n_tokens + n_new tokens.  bf16 contexts only.
+ * Errors: as crf_recompute_window over the window [0, N) of a prefix of
+ * n_tokens + n_new tokens, plus SHAPE (n_new < 1), UNSUPPORTED (fp32 context,
+ * vocab not a positive multiple of 8, LM head of 2 GiB or more), WORKSPACE
+ * (n_new or n_tokens + n_new above max_tokens), INVALID_ARG (NULL or
+ * misaligned final_norm, lm_head, logits_out). */
+crf_status crf_decode_logits(crf_context *ctx, const crf_model_dims *dims, const void *new_tokens, int32_t n_new,
+                             const crf_layer_weights *base_weights, const crf_lora_layer *lora,
+                             const crf_kv_cache *kv_cache, const void *final_norm, const void *lm_head,
+                             int32_t vocab, float *logits_out, void *stream);
+
 /* Runtime drift and risk (Sec. 4.1 "Runtime risk and range selection", Eq. 8):
  *   d_l = || theta_t - theta_l^anchor ||_2,   q_l = s_l * d_l.
  * theta is the whole adapter: every A and B entry of every target of every

@@ -87,6 +87,19 @@ def rope(x: np.ndarray, theta: float) -> np.ndarray:
     return np.concatenate([x1 * c - x2 * s, x2 * c + x1 * s], axis=-1)
 
 
+def rope_at(x: np.ndarray, positions: np.ndarray, theta: float) -> np.ndarray:
+    """The same rotation at arbitrary absolute positions (x [m, heads, hd],
+    positions [m]): phi[j, i] = positions[j] * theta^(-2i/hd)."""
+    x = _f64(x)
+    hd = x.shape[-1]
+    half = hd // 2
+    inv_freq = theta ** (-(2.0 * np.arange(half, dtype=F)) / hd)
+    phi = _f64(positions)[:, None] * inv_freq[None, :]
+    c, s = np.cos(phi)[:, None, :], np.sin(phi)[:, None, :]
+    x1, x2 = x[..., :half], x[..., half:]
+    return np.concatenate([x1 * c - x2 * s, x2 * c + x1 * s], axis=-1)
+
+
 def causal_gqa_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, q_block: int = 1024) -> np.ndarray:
     """Standard causal softmax self-attention with grouped K/V heads (Sec. 2.1 KV
     caching; Sec. 5 setup).  q [n, nq, hd], k/v [n, nkv, hd] -> [n, nq, hd].
@@ -179,6 +192,81 @@ def recompute_window(hidden_at_boundary: np.ndarray, weights: Mapping[int, Mappi
 def prefill(embeddings: np.ndarray, weights, lora, dims, lora_scale: float = 1.0):
     """Fresh full-prefill recomputation: all N layers from H_{-1} (Sec. 2.2)."""
     return recompute_window(embeddings, weights, lora, 0, dims.n_layers, dims, lora_scale, keep_hidden=True)
+
+
+# ----------------------------------------------------------------------------- first decoding step
+
+def decode_layer(h_new: np.ndarray, cache_k: np.ndarray, cache_v: np.ndarray, w: Mapping[str, np.ndarray],
+                 lora: Optional[LoraLayer], dims, lora_scale: float = 1.0):
+    """One decoder layer for m new tokens at positions n..n+m-1 on top of a cached
+    prefix of n tokens (Sec. 2.1 KV caching): the new tokens attend to the cached
+    K/V of this layer, whatever adapter version produced them, and causally to
+    themselves.  Returns (H_l rows of the new tokens, their K_l, V_l)."""
+    lora = lora or {}
+    h = _f64(h_new)
+    m = h.shape[0]
+    n = cache_k.shape[0]
+    nq, nkv, hd = dims.n_q_heads, dims.n_kv_heads, dims.head_dim
+
+    def lin(x, t, bias=None):
+        return lora_linear(x, w["w_" + t], lora.get(t), lora_scale, bias)
+
+    x = rms_norm(h, w["attn_norm"], dims.rms_eps)
+    pos = np.arange(n, n + m)
+    q = rope_at(lin(x, "q", w.get("bias_q")).reshape(m, nq, hd), pos, dims.rope_theta)
+    k = rope_at(lin(x, "k", w.get("bias_k")).reshape(m, nkv, hd), pos, dims.rope_theta)
+    v = lin(x, "v", w.get("bias_v")).reshape(m, nkv, hd)
+    kk = np.concatenate([_f64(cache_k), k], axis=0)
+    vv = np.concatenate([_f64(cache_v), v], axis=0)
+    rep = nq // nkv
+    o = np.empty((m, nq, hd), dtype=F)
+    for i in range(m):
+        visible = n + i + 1                       # prefix plus new tokens 0..i
+        for j in range(nq):
+            g = j // rep
+            sc = (kk[:visible, g, :] @ q[i, j, :]) / math.sqrt(hd)
+            sc = np.exp(sc - sc.max())
+            o[i, j, :] = (sc / sc.sum()) @ vv[:visible, g, :]
+    h = h + lin(o.reshape(m, nq * hd), "o")
+    x2 = rms_norm(h, w["mlp_norm"], dims.rms_eps)
+    h = h + lin(silu(lin(x2, "gate")) * lin(x2, "up"), "down")
+    return h, k, v
+
+
+def decode_logits(x_new: np.ndarray, caches: Mapping[int, Tuple[np.ndarray, np.ndarray]], weights, lora, dims,
+                  final_norm: np.ndarray, lm_head: np.ndarray, lora_scale: float = 1.0) -> np.ndarray:
+    """First-step next-token logits (Sec. 3.2 "Tail Influence", z): the new
+    tokens' embeddings run through all N layers over the cache (caches[l] =
+    (K_l, V_l) of the prefix, possibly a mix of refreshed and historical
+    layers), then the final RMSNorm and the LM head on the last new token."""
+    h = _f64(x_new)
+    for l in range(dims.n_layers):
+        k, v = caches[l]
+        h, _, _ = decode_layer(h, k, v, weights[l], lora.get(l), dims, lora_scale)
+    hf = rms_norm(h[-1:], final_norm, dims.rms_eps)
+    return (hf @ _f64(lm_head).T)[0]
+
+
+def hybrid_caches(fresh: Mapping[int, Tuple], stale: Mapping[int, Tuple], b: int, n_layers: int):
+    """Cache of boundary b: refreshed states before layer b, historical ones at b..N-1."""
+    return {l: (fresh[l] if l < b else stale[l]) for l in range(n_layers)}
+
+
+def tail_influence(z_by_boundary: Sequence[np.ndarray]) -> np.ndarray:
+    """v_l = z^(l) - z^(l+1) and T_b = sum_{l >= b} ||v_l||_2 for b = 0..N (Eq.
+    tail-influence); z_by_boundary[b] = z^(b), with z^(N) the fresh logits."""
+    z = [_f64(x) for x in z_by_boundary]
+    n = len(z) - 1
+    norms = np.array([np.linalg.norm(z[l] - z[l + 1]) for l in range(n)])
+    return np.concatenate([np.cumsum(norms[::-1])[::-1], [0.0]])
+
+
+def kl_divergence(z_ref: np.ndarray, z: np.ndarray) -> float:
+    """KL(softmax(z_ref) || softmax(z)) from logits, in log-sum-exp form."""
+    a, b = _f64(z_ref), _f64(z)
+    la = a - (a.max() + np.log(np.exp(a - a.max()).sum()))
+    lb = b - (b.max() + np.log(np.exp(b - b.max()).sum()))
+    return float(np.sum(np.exp(la) * (la - lb)))
 
 
 # ----------------------------------------------------------------------------- paging

@@ -69,7 +69,7 @@ _LIB: Optional[ctypes.CDLL] = None
 EXPORTS = ("crf_status_string", "crf_abi_version", "crf_context_create", "crf_context_destroy", "crf_last_error",
            "crf_validate_dims", "crf_validate_window", "crf_recompute_window", "crf_recompute_window_batched",
            "crf_layer_drift", "crf_context_device_errors", "crf_context_set_timing", "crf_context_read_timing",
-           "crf_device_info")
+           "crf_device_info", "crf_decode_logits")
 
 
 def load(path: str = LIB_PATH) -> ctypes.CDLL:
@@ -108,6 +108,9 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.crf_context_set_timing.argtypes = [VP, I32]
     lib.crf_context_read_timing.restype = I32
     lib.crf_context_read_timing.argtypes = [VP, P(ctypes.c_float), P(I32), I32]
+    lib.crf_decode_logits.restype = I32
+    lib.crf_decode_logits.argtypes = [VP, P(ModelDims), VP, I32, P(LayerWeights), P(LoraLayer), P(KVCache), VP, VP,
+                                      I32, VP, VP]
     lib.crf_device_info.restype = I32
     lib.crf_device_info.argtypes = [I32, P(I32), P(I32), ctypes.c_char_p, I32]
     _LIB = lib
@@ -284,6 +287,17 @@ def recompute_window_batched(ctx: Context, dims: ModelDims, base_weights: ctypes
     st = ctx.lib.crf_recompute_window_batched(ctx.handle, ctypes.byref(dims), base_weights, len(items), arr,
                                               _stream(stream))
     _err(ctx.lib, ctx.handle, st)
+
+
+def decode_logits(ctx: Context, dims: ModelDims, new_tokens, base_weights: ctypes.Array,
+                  lora: Optional[ctypes.Array], kv: KVCache, final_norm, lm_head, logits_out, stream=None):
+    """crf_decode_logits: first-step next-token logits of the last of new_tokens
+    [n_new, d] over the cached prefix kv (kv.n_tokens tokens)."""
+    lib = ctx.lib
+    st = lib.crf_decode_logits(ctx.handle, ctypes.byref(dims), _ptr(new_tokens), int(new_tokens.shape[0]),
+                               base_weights, lora, ctypes.byref(kv), _ptr(final_norm), _ptr(lm_head),
+                               int(lm_head.shape[0]), _ptr(logits_out), _stream(stream))
+    _err(lib, ctx.handle, st)
 
 
 def layer_drift(ctx: Context, dims: ModelDims, current: ctypes.Array, versions: Sequence[ctypes.Array],

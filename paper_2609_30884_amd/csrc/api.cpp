@@ -240,11 +240,15 @@ bool has_lora(const crf_lora_layer *lora, int l, int t) {
   return lora && lora[l].rank > 0 && lora[l].A[t] != nullptr;
 }
 
+// Layers [l0, l0+h) over `rows` token rows at positions pos0..pos0+rows-1: a
+// window (pos0 = 0, rows = the prefix) or new tokens over a cached prefix
+// (pos0 = the prefix length).  kv_tail: without hidden_out the last layer runs
+// its K/V projections only.
 crf_status run_layers_bf16(crf_context *ctx, const void *hb, const crf_layer_weights *W,
                            const crf_lora_layer *lora, int l0, int h, const crf_kv_cache *kv, void *hout,
-                           hipStream_t s) {
+                           hipStream_t s, int rows, int pos0, bool kv_tail) {
   const crf_model_dims &d = ctx->dims;
-  const int M = kv->n_tokens, D = d.d_model, dq = dq_of(d), dkv = dkv_of(d), f = d.d_ffn, hd = d.head_dim;
+  const int M = rows, D = d.d_model, dq = dq_of(d), dkv = dkv_of(d), f = d.d_ffn, hd = d.head_dim;
   const int rp = ctx->rank_pad, ldu = 3 * rp;
   bf16 *xn = (bf16 *)ctx->xn, *q = (bf16 *)ctx->q, *attn = (bf16 *)ctx->attn, *act = (bf16 *)ctx->act;
   bf16 *u = (bf16 *)ctx->u;
@@ -276,6 +280,7 @@ crf_status run_layers_bf16(crf_context *ctx, const void *hb, const crf_layer_wei
       p.kpad = rp;
       p.rank = rank;
       p.rope_cs = ctx->rope_cs;
+      p.pos0 = pos0;
       return p;
     };
     LoraDownTarget tg[3];
@@ -284,7 +289,7 @@ crf_status run_layers_bf16(crf_context *ctx, const void *hb, const crf_layer_wei
     LAUNCH(ctx, s, CRF_KK_NORM,
            launch_rmsnorm(s, first ? hb : (const void *)ctx->hres, !first, w.attn_norm, false, xn, false,
                           first ? ctx->hres : nullptr, M, D, d.rms_eps));
-    if (last && !hout) {
+    if (last && !hout && kv_tail) {
       // Nothing reads this layer's output: its cache entry depends only on its
       // input through the K and V projections, so only those run.
       const bool kv_any = lora_targets({CRF_K, CRF_V}, tg);
@@ -334,7 +339,8 @@ crf_status run_layers_bf16(crf_context *ctx, const void *hb, const crf_layer_wei
       p.kv = layer_kv(ctx, kv, l);
       LAUNCH(ctx, s, CRF_KK_GEMM_QKV, launch_gemm_bf16(s, EPI_QKV, hd, p));
     }
-    LAUNCH(ctx, s, CRF_KK_ATTN, launch_attn_bf16(s, q, layer_kv(ctx, kv, l), attn, M, d.n_q_heads, d.n_kv_heads, hd));
+    LAUNCH(ctx, s, CRF_KK_ATTN,
+           launch_attn_bf16(s, q, layer_kv(ctx, kv, l), attn, M, pos0, d.n_q_heads, d.n_kv_heads, hd));
     any = lora_targets({CRF_O}, tg);
     if (any) LAUNCH(ctx, s, CRF_KK_LORA_DOWN, launch_lora_down_bf16(s, attn, dq, M, dq, tg, 1, rp, u, ldu));
     {
@@ -441,7 +447,7 @@ crf_status run_layers_f32(crf_context *ctx, const void *hb, const crf_layer_weig
 crf_status run_window(crf_context *ctx, const void *hb, const crf_layer_weights *W, const crf_lora_layer *lora,
                       int l0, int h, const crf_kv_cache *kv, void *hout, hipStream_t s) {
   if (h == 0 || kv->n_tokens == 0) return CRF_OK;
-  if (ctx->dims.dtype == CRF_BF16) return run_layers_bf16(ctx, hb, W, lora, l0, h, kv, hout, s);
+  if (ctx->dims.dtype == CRF_BF16) return run_layers_bf16(ctx, hb, W, lora, l0, h, kv, hout, s, kv->n_tokens, 0, true);
   return run_layers_f32(ctx, hb, W, lora, l0, h, kv, hout, s);
 }
 
@@ -571,6 +577,54 @@ crf_status crf_recompute_window_batched(crf_context *ctx, const crf_model_dims *
                                (hipStream_t)stream);
     if (st != CRF_OK) return st;
   }
+  return CRF_OK;
+}
+
+crf_status crf_decode_logits(crf_context *ctx, const crf_model_dims *dims, const void *new_tokens, int32_t n_new,
+                             const crf_layer_weights *base_weights, const crf_lora_layer *lora,
+                             const crf_kv_cache *kv_cache, const void *final_norm, const void *lm_head,
+                             int32_t vocab, float *logits_out, void *stream) {
+  if (!ctx) return fail(nullptr, CRF_ERR_INVALID_ARG, "context is NULL");
+  const char *what = "crf_decode_logits";
+  if (!kv_cache) return fail(ctx, CRF_ERR_INVALID_ARG, "%s: kv_cache is NULL", what);
+  if (n_new < 1) return fail(ctx, CRF_ERR_SHAPE, "%s: n_new must be >= 1", what);
+  if (ctx->dims.dtype != CRF_BF16) return fail(ctx, CRF_ERR_UNSUPPORTED, "%s: bf16 contexts only", what);
+  // every layer, over the prefix plus the new tokens (their slots are written)
+  crf_kv_cache ext = *kv_cache;
+  ext.n_tokens = kv_cache->n_tokens + n_new;
+  crf_status st = check_request(ctx, dims, new_tokens, base_weights, lora, 0, ctx->dims.n_layers, &ext, nullptr,
+                                what);
+  if (st != CRF_OK) return st;
+  if (n_new > ctx->max_tokens)
+    return fail(ctx, CRF_ERR_WORKSPACE, "%s: n_new %d exceeds the context's max_tokens", what, n_new);
+  if (vocab < 8 || vocab % 8)
+    return fail(ctx, CRF_ERR_UNSUPPORTED, "%s: vocab must be a positive multiple of 8 (got %d)", what, vocab);
+  if ((int64_t)vocab * ctx->dims.d_model * 2 >= (int64_t)CRF_OOB)
+    return fail(ctx, CRF_ERR_UNSUPPORTED, "%s: LM head larger than 2 GiB", what);
+  if (!final_norm || !lm_head || !logits_out || !aligned16(final_norm) || !aligned16(lm_head) ||
+      !aligned16(logits_out))
+    return fail(ctx, CRF_ERR_INVALID_ARG, "%s: final_norm, lm_head or logits_out NULL or misaligned", what);
+  hipStream_t s = (hipStream_t)stream;
+  const crf_model_dims &d = ctx->dims;
+  st = run_layers_bf16(ctx, new_tokens, base_weights, lora, 0, d.n_layers, &ext, nullptr, s, n_new,
+                       kv_cache->n_tokens, false);
+  if (st != CRF_OK) return st;
+  // final RMSNorm of the last new token (fp32 residual stream) and the LM head
+  const size_t D = d.d_model;
+  LAUNCH(ctx, s, CRF_KK_NORM,
+         launch_rmsnorm(s, ctx->hres + (size_t)(n_new - 1) * D, true, final_norm, false, ctx->xn, false, nullptr, 1,
+                        (int)D, d.rms_eps));
+  GemmParams p{};
+  p.X = (const bf16 *)ctx->xn;
+  p.ldx = D;
+  p.M = 1;
+  p.K = (int)D;
+  p.N = vocab;
+  p.w[0] = (const bf16 *)lm_head;
+  p.resid = logits_out;
+  p.ldr = vocab;
+  p.resid_overwrite = 1;
+  LAUNCH(ctx, s, CRF_KK_OTHER, launch_gemm_bf16(s, EPI_RESID, d.head_dim, p));
   return CRF_OK;
 }
 

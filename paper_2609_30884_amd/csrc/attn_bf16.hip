@@ -84,8 +84,8 @@ struct PageMap {
 // XCD: balanced per-XCD KV-head mapping (R = 8 / nkv XCDs per KV head).
 template <int HD, int PS>
 __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16 *__restrict__ Q, PagedKV kv,
-                                                           bf16 *__restrict__ O, int M, int nq, int nkv,
-                                                           uint32_t pool_bytes, int xcd_r) {
+                                                           bf16 *__restrict__ O, int Mq, int q_off, int nq,
+                                                           int nkv, uint32_t pool_bytes, int xcd_r) {
   constexpr int CH = HD / 8;             // 16-byte chunks per row
   constexpr int KS = HD / 16;            // MFMA k-steps for S
   constexpr int HB = HD / 32;            // 32-row hd blocks of O^T
@@ -97,7 +97,11 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16 *__restric
   __shared__ __align__(16) bf16 ks0[TILE], ks1[TILE], vs0[TILE], vs1[TILE];
   __shared__ uint32_t pgbase[PGCAP];
 
-  const int nqb = (M + BQ - 1) / BQ;
+  // Query rows 0..Mq-1 sit at positions q_off..q_off+Mq-1 and attend to keys
+  // 0..q_off+row: the cached prefix and the rows before them (q_off = 0 and
+  // Mq = the prefix length for a window).
+  const int M = q_off + Mq;  // keys
+  const int nqb = (Mq + BQ - 1) / BQ;
   const int group = nq / nkv;
   int head, qblk;
   if (xcd_r > 0) {
@@ -122,7 +126,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16 *__restric
 
   bf16x8 qf[KS];
   {
-    const bf16 *qrow = Q + (int64_t)min(qi, M - 1) * dq + head * HD + 8 * g;
+    const bf16 *qrow = Q + (int64_t)min(qi, Mq - 1) * dq + head * HD + 8 * g;
 #pragma unroll
     for (int s = 0; s < KS; ++s) qf[s] = as_bf16x8(ld16(qrow + 16 * s));
   }
@@ -132,7 +136,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16 *__restric
   const PageMap pm{kv.block_table, kv.n_pages, (uint32_t)(kv.page_stride * 2), (uint32_t)(g_kv * ps * HD * 2),
                    kv.err};
 
-  const int last_key = min(q0 + BQ, M) - 1;
+  const int last_key = min(q_off + q0 + BQ, M) - 1;
   const int ntiles = last_key / BKV + 1;
   const int n_pages_needed = last_key / ps + 1;
 
@@ -227,7 +231,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16 *__restric
       }
       dma(kt0 + BKV, kn, vn);
     }
-    if (kt0 > q0w + 31) return;  // every key of this tile is in this wave's future
+    if (kt0 > q_off + q0w + 31) return;  // every key of this tile is in this wave's future
     f32x16 sacc[2];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
@@ -254,13 +258,13 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16 *__restric
       __builtin_amdgcn_sched_barrier(0);
     }
     // causal mask (also hides keys >= M, which are always > qi for valid qi)
-    if (kt0 + BKV - 1 > q0w) {
+    if (kt0 + BKV - 1 > q_off + q0w) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
           const int key = kt0 + kb * 32 + 8 * (v / 4) + 4 * g + (v % 4);
-          if (key > qi) sacc[kb][v] = -INFINITY;
+          if (key > q_off + qi) sacc[kb][v] = -INFINITY;
         }
     }
     float mx = -INFINITY;
@@ -318,7 +322,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16 *__restric
   }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
-  if (qi >= M) return;
+  if (qi >= Mq) return;
   const float inv = 1.0f / l_tot;
   bf16 *orow = O + (int64_t)qi * dq + head * HD;
 #pragma unroll
@@ -332,32 +336,34 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16 *__restric
 }
 
 template <int HD>
-void launch(hipStream_t s, const bf16 *Q, const PagedKV &kv, bf16 *O, int M, int nq, int nkv, uint32_t pool_bytes) {
-  const int nqb = (M + BQ - 1) / BQ;
+void launch(hipStream_t s, const bf16 *Q, const PagedKV &kv, bf16 *O, int Mq, int q_off, int nq, int nkv,
+            uint32_t pool_bytes) {
+  const int nqb = (Mq + BQ - 1) / BQ;
   int xcd_r = 0, grid = nqb * nq;
   if (nkv <= 8 && 8 % nkv == 0) {
     xcd_r = 8 / nkv;
     grid = 8 * (nq / nkv) * ((nqb + xcd_r - 1) / xcd_r);
   }
   if (kv.page_size == 16)
-    hipLaunchKernelGGL((attn_bf16_kernel<HD, 16>), dim3(grid), dim3(256), 0, s, Q, kv, O, M, nq, nkv, pool_bytes,
+    hipLaunchKernelGGL((attn_bf16_kernel<HD, 16>), dim3(grid), dim3(256), 0, s, Q, kv, O, Mq, q_off, nq, nkv, pool_bytes,
                        xcd_r);
   else
-    hipLaunchKernelGGL((attn_bf16_kernel<HD, 0>), dim3(grid), dim3(256), 0, s, Q, kv, O, M, nq, nkv, pool_bytes,
+    hipLaunchKernelGGL((attn_bf16_kernel<HD, 0>), dim3(grid), dim3(256), 0, s, Q, kv, O, Mq, q_off, nq, nkv, pool_bytes,
                        xcd_r);
 }
 
 }  // namespace
 
-hipError_t launch_attn_bf16(hipStream_t s, const bf16 *Q, const PagedKV &kv, bf16 *O, int M, int nq, int nkv,
-                            int hd) {
-  if (M <= 0) return hipSuccess;
+hipError_t launch_attn_bf16(hipStream_t s, const bf16 *Q, const PagedKV &kv, bf16 *O, int Mq, int q_off, int nq,
+                            int nkv, int hd) {
+  if (Mq <= 0) return hipSuccess;
+  if (q_off < 0) return hipErrorInvalidValue;
   const int64_t bytes = (int64_t)kv.n_pages * kv.page_stride * 2;
   if (bytes >= (int64_t)CRF_OOB) return hipErrorInvalidValue;
   if (hd == 128)
-    launch<128>(s, Q, kv, O, M, nq, nkv, (uint32_t)bytes);
+    launch<128>(s, Q, kv, O, Mq, q_off, nq, nkv, (uint32_t)bytes);
   else if (hd == 64)
-    launch<64>(s, Q, kv, O, M, nq, nkv, (uint32_t)bytes);
+    launch<64>(s, Q, kv, O, Mq, q_off, nq, nkv, (uint32_t)bytes);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

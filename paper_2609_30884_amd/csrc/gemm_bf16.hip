@@ -274,7 +274,7 @@ __global__ __launch_bounds__(64 * WAVES, 1) void gemm_bf16_kernel(const GemmPara
           const int n = n0 + wn * 128 + 32 * i + 8 * ii + 4 * g;
           if (n >= p.N) continue;
           float *rp = p.resid + (int64_t)m * p.ldr + n;
-          f32x4 r = *reinterpret_cast<f32x4 *>(rp);
+          f32x4 r = p.resid_overwrite ? f32x4{0.f, 0.f, 0.f, 0.f} : *reinterpret_cast<f32x4 *>(rp);
 #pragma unroll
           for (int jj = 0; jj < 4; ++jj) r[jj] += acc[i][j][ii * 4 + jj];
           *reinterpret_cast<f32x4 *>(rp) = r;
@@ -316,8 +316,8 @@ __global__ __launch_bounds__(64 * WAVES, 1) void gemm_bf16_kernel(const GemmPara
       if (m >= p.M || fb >= p.N) continue;
       int64_t prow[HPW];
 #pragma unroll
-      for (int hh = 0; hh < HPW; ++hh) prow[hh] = sg ? paged_row(p.kv, m, head0 + hh, HD) : 0;
-      const float2 *cs = p.rope_cs + (int64_t)m * (HD / 2);
+      for (int hh = 0; hh < HPW; ++hh) prow[hh] = sg ? paged_row(p.kv, p.pos0 + m, head0 + hh, HD) : 0;
+      const float2 *cs = p.rope_cs + (int64_t)(p.pos0 + m) * (HD / 2);
 #pragma unroll
       for (int hh = 0; hh < HPW; ++hh)
 #pragma unroll

@@ -59,18 +59,22 @@ struct GemmParams {
   int dq;
   PagedKV kv;
   const float2 *rope_cs;
-  // EPI_RESID: resid[m, n] += acc; resid_out (nullable) = bf16(resid)
+  // EPI_QKV: token row m sits at position pos0 + m (rotary angle and page slot)
+  int pos0;
+  // EPI_RESID: resid[m, n] += acc (= acc when resid_overwrite); resid_out (nullable) = bf16(resid)
   float *resid;
   bf16 *resid_out;
   int ldr;
+  int resid_overwrite;
   // EPI_SWIGLU: act[m, f] = silu(gate) * up
   bf16 *act;
   int d_ffn;
 };
 hipError_t launch_gemm_bf16(hipStream_t s, GemmEpi epi, int hd, const GemmParams &p);
 
-hipError_t launch_attn_bf16(hipStream_t s, const bf16 *Q, const PagedKV &kv, bf16 *O, int M, int nq, int nkv,
-                            int hd);
+// Query rows 0..Mq-1 at positions q_off..q_off+Mq-1 over keys 0..q_off+Mq-1.
+hipError_t launch_attn_bf16(hipStream_t s, const bf16 *Q, const PagedKV &kv, bf16 *O, int Mq, int q_off, int nq,
+                            int nkv, int hd);
 
 // ---------------------------------------------------------------- drift
 struct DriftSeg {

@@ -141,6 +141,7 @@ def to_storage(x: np.ndarray, dtype: str) -> np.ndarray:
 _TENSOR_IDS = {
     "hidden": 1, "attn_norm": 2, "mlp_norm": 3, "block_table": 4, "sensitivity": 5,
     "anchors": 6, "canary": 7, "bias_q": 8, "bias_k": 9, "bias_v": 10,
+    "new_tokens": 11, "final_norm": 12, "lm_head": 13,
 }
 for _i, _t in enumerate(TARGETS):
     _TENSOR_IDS["w_" + _t] = 20 + _i
@@ -170,6 +171,20 @@ def gen_hidden(wl: Workload, seed: int, n_tokens: int, item: int = 0) -> np.ndar
     """Boundary hidden state H_{l0-1} ~ N(0,1), [n_tokens, d_model]."""
     rng = rng_for(seed, wl.config_id, -1, "hidden", item)
     return to_storage(_normal(rng, (n_tokens, wl.dims.d_model), 1.0), wl.dims.dtype)
+
+
+def gen_new_tokens(wl: Workload, seed: int, n_new: int, item: int = 0) -> np.ndarray:
+    """Embedding states of tokens appended after the cached prefix, N(0,1), [n_new, d_model]."""
+    rng = rng_for(seed, wl.config_id, -1, "new_tokens", item)
+    return to_storage(_normal(rng, (n_new, wl.dims.d_model), 1.0), wl.dims.dtype)
+
+
+def gen_head(wl: Workload, seed: int, vocab: int) -> Tuple[np.ndarray, np.ndarray]:
+    """Final RMSNorm gain 1 + N(0, 0.02) [d_model] and LM head N(0, 0.02) [vocab, d_model]."""
+    d = wl.dims.d_model
+    g = to_storage(_normal(rng_for(seed, wl.config_id, -1, "final_norm"), (d,), 0.02, 1.0), wl.dims.dtype)
+    w = to_storage(_normal(rng_for(seed, wl.config_id, -1, "lm_head"), (vocab, d), 0.02), wl.dims.dtype)
+    return g, w
 
 
 def gen_layer_weights(wl: Workload, seed: int, layer: int, with_bias: bool = False) -> Dict[str, np.ndarray]:
