@@ -11,7 +11,8 @@ Other workloads (one JSON line each): tiny_f32, qwen15b_4k, qwen7b_16k_suffix
 (the 24-layer affected suffix), qwen15b_mixed8 (8 ragged stale caches through
 the batched call), drift (crf_layer_drift over 28 layers and 4 stored
 adapter versions at 1.5B shapes), trajectory (maintenance over 32 adapter
-updates: fresh, exact suffix, drift policy, reuse) and copy (a 1 GiB
+updates: fresh, exact suffix, drift policy, reuse), tail (first-step logits
+over hybrid caches at every boundary, timed decoding step) and copy (a 1 GiB
 elementwise pass that calibrates the HBM byte counters).
 """
 from __future__ import annotations
@@ -153,6 +154,8 @@ def main():
         return bench_copy(args)
     if args.workload == "trajectory":
         return bench_trajectory(args)
+    if args.workload == "tail":
+        return bench_tail(args)
     wl = syn.WORKLOADS[args.workload]
     dims = wl.dims
     win = wl.window
@@ -429,6 +432,92 @@ def bench_trajectory(args):
                       "updates": [f"{t}@{l}" for l, t in setup.updates]},
            "strategies": summ,
            "sensitivity": [round(float(x), 4) for x in sens.cpu()]}
+    print(json.dumps(out), flush=True)
+
+
+def bench_tail(args):
+    """Tail influence at the 7B shapes (Sec. 3.2): the first-step logits z^(b)
+    of one new token over a 16K-token prefix whose cache layers before b are
+    refreshed under the current adapter and from b on come from an older one,
+    for every boundary b = 0..N; the decoding step is timed (HBM-bound)."""
+    import numpy as np
+    import torch
+    import paper_2609_30884_amd as crf
+    import synthetic as syn
+    from synthetic.trajectory import make_setup, make_state_buffers
+    vocab = 152064
+    wl = syn.WORKLOADS["qwen7b_16k"]
+    dims, n = wl.dims, wl.window.n_tokens
+    N = dims.n_layers
+    t0 = time.perf_counter()
+    setup = make_setup(wl, args.seed, n + 1, 0)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(args.seed + 2)
+    cur = []
+    for ll in setup.base_lora:   # the current adapter: every B factor moved by N(0, 0.02)
+        tg = {t: (a, (b.float() + 0.02 * torch.randn(b.shape, generator=g, device="cuda")).to(torch.bfloat16))
+              for t, (a, b) in ll["targets"].items()}
+        cur.append({"rank": ll["rank"], "scale": ll["scale"], "targets": tg})
+    fnorm = (1.0 + 0.02 * torch.randn(dims.d_model, generator=g, device="cuda")).to(torch.bfloat16)
+    head = (0.02 * torch.randn((vocab, dims.d_model), generator=g, device="cuda")).to(torch.bfloat16)
+    x_new = setup.embedding[n:n + 1].contiguous()
+    emb = setup.embedding[:n].contiguous()
+    cd = crf.make_dims(N, dims.d_model, dims.n_q_heads, dims.n_kv_heads, dims.head_dim, dims.d_ffn,
+                       dims.rms_eps, dims.rope_theta, dims.dtype)
+    ctx = crf.Context(cd, n + 1, wl.lora_rank)
+    weights = crf.layer_weights_array(setup.weights)
+    lo_cur, lo_old = crf.lora_array(cur, N), crf.lora_array(setup.base_lora, N)
+    pools = {}
+    for name, lo in (("fresh", lo_cur), ("stale", lo_old)):
+        k, v, _ = make_state_buffers(setup, wl.page_size)
+        kv = crf.kv_cache(k, v, setup.block_table, n, wl.page_size)
+        crf.recompute_window(ctx, cd, emb, weights, lo, 0, N, kv, None)
+        pools[name] = (k, v)
+    hk, hv = pools["stale"][0].clone(), pools["stale"][1].clone()
+    kvh = crf.kv_cache(hk, hv, setup.block_table, n, wl.page_size)
+    logits = torch.empty(vocab, dtype=torch.float32, device="cuda")
+    torch.cuda.synchronize()
+    print(f"[bench] tail set-up and prefills in {time.perf_counter() - t0:.1f}s", file=sys.stderr, flush=True)
+    zs, times = [], []
+    for b in range(N + 1):
+        if b > 0:   # boundary b: layer b-1 now refreshed
+            hk[b - 1].copy_(pools["fresh"][0][b - 1])
+            hv[b - 1].copy_(pools["fresh"][1][b - 1])
+        for _ in range(max(1, args.warmup) if b == 0 else 0):
+            crf.decode_logits(ctx, cd, x_new, weights, lo_cur, kvh, fnorm, head, logits)
+        torch.cuda.synchronize()
+        reps = max(1, args.steps // 4)
+        t1 = time.perf_counter()
+        for _ in range(reps):
+            crf.decode_logits(ctx, cd, x_new, weights, lo_cur, kvh, fnorm, head, logits)
+        torch.cuda.synchronize()
+        times.append((time.perf_counter() - t1) / reps)
+        zs.append(logits.double().cpu().numpy())
+    assert ctx.device_errors() == 0
+    z_star = zs[-1]
+    v = [np.linalg.norm(zs[l] - zs[l + 1]) for l in range(N)]
+    T = [float(sum(v[b:])) for b in range(N + 1)]
+
+    def kl(a, c):
+        la = a - (a.max() + np.log(np.exp(a - a.max()).sum()))
+        lc = c - (c.max() + np.log(np.exp(c - c.max()).sum()))
+        return float(np.sum(np.exp(la) * (la - lc)))
+    kls = [kl(z_star, z) for z in zs]
+    top1 = [bool(np.argmax(z) == np.argmax(z_star)) for z in zs]
+    ms = 1e3 * float(np.median(times))
+    w_bytes = N * 2 * (dims.d_model * (dims.dq + 2 * dims.dkv) + dims.dq * dims.d_model + 3 * dims.d_model * dims.d_ffn)
+    bytes_step = w_bytes + vocab * dims.d_model * 2 + N * 2 * n * dims.dkv * 2
+    out = {"metric": "first-step decode latency over a 16K-token hybrid cache (7B shapes, 152064-token head)",
+           "value": round(ms, 3), "unit": "ms", "n_gpus": 1, "steps": N + 1, "warmup": args.warmup,
+           "ms_per_step": round(ms, 3), "higher_is_better": False, "scaling": "weak", "vs_baseline": None,
+           "dtype": "bf16", "data": "synthetic (seeded device draws; current adapter = every B + N(0, 0.02))",
+           "config": {"workload": f"tail: one new token over a {n}-token prefix, {N} layers, hybrid boundary b = 0..{N}",
+                      "vocab": vocab},
+           "roofline": {"bound": "hbm", "kernel": "decode step (all kernels)",
+                        "achieved": round(bytes_step / (ms * 1e-3) / 1e9, 1), "peak": PEAK_HBM / 1e9, "unit": "GB/s",
+                        "frac": round(bytes_step / (ms * 1e-3) / PEAK_HBM, 4), "traffic": None},
+           "tail": {"T_b": [round(x, 4) for x in T], "kl": [float(f"{x:.4g}") for x in kls],
+                    "kl_bound_holds": all(k <= 0.25 * t * t + 1e-9 for k, t in zip(kls, T)), "top1_agree": top1}}
     print(json.dumps(out), flush=True)
 
 
