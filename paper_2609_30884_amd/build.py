@@ -19,7 +19,8 @@ OBJ = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libcrf.so")
 ARCH = "gfx950"
 
-SOURCES = ["api.cpp", "norm.hip", "f32_path.hip", "lora_down.hip", "gemm_bf16.hip", "attn_bf16.hip", "drift.hip"]
+SOURCES = ["api.cpp", "norm.hip", "f32_path.hip", "lora_down.hip", "gemm_bf16.hip", "gemm_skinny.hip",
+           "attn_bf16.hip", "drift.hip"]
 
 CFLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function",

@@ -43,6 +43,9 @@ struct crf_context {
   float *gu = nullptr;     // fp32 path: [T, 2f]
   float2 *rope_cs = nullptr;
   int *d_err = nullptr;
+  float *proj16 = nullptr;  // bf16 path, <= 16 token rows: fp32 Q/K/V projections [16, dq + 2 dkv]
+  float *attn_part = nullptr;  // bf16 path, <= 16 query rows: key-split attention partials
+  int64_t attn_part_floats = 0;
   // drift staging
   void *drift_host = nullptr;
   size_t drift_host_bytes = 0;
@@ -284,6 +287,13 @@ crf_status run_layers_bf16(crf_context *ctx, const void *hb, const crf_layer_wei
       return p;
     };
     LoraDownTarget tg[3];
+    // a few token rows (a decoding step, a very short window): weight-streaming kernels
+    const bool skinny = M <= 16;
+    auto gemm = [&](GemmEpi epi, GemmParams &p) {
+      if (!skinny) return launch_gemm_bf16(s, epi, hd, p);
+      p.proj = ctx->proj16;
+      return launch_gemm_skinny_bf16(s, epi, hd, p);
+    };
 
     // attention block
     LAUNCH(ctx, s, CRF_KK_NORM,
@@ -311,7 +321,7 @@ crf_status run_layers_bf16(crf_context *ctx, const void *hb, const crf_layer_wei
       p.bias[2] = (const bf16 *)w.bias_v;
       p.dq = dq;
       p.kv = layer_kv(ctx, kv, l);
-      LAUNCH(ctx, s, CRF_KK_GEMM_QKV, launch_gemm_bf16(s, EPI_QKV, hd, p));
+      LAUNCH(ctx, s, CRF_KK_GEMM_QKV, gemm(EPI_QKV, p));
       break;
     }
     bool any = lora_targets({CRF_Q, CRF_K, CRF_V}, tg);
@@ -337,10 +347,11 @@ crf_status run_layers_bf16(crf_context *ctx, const void *hb, const crf_layer_wei
       p.q_out = q;
       p.dq = dq;
       p.kv = layer_kv(ctx, kv, l);
-      LAUNCH(ctx, s, CRF_KK_GEMM_QKV, launch_gemm_bf16(s, EPI_QKV, hd, p));
+      LAUNCH(ctx, s, CRF_KK_GEMM_QKV, gemm(EPI_QKV, p));
     }
     LAUNCH(ctx, s, CRF_KK_ATTN,
-           launch_attn_bf16(s, q, layer_kv(ctx, kv, l), attn, M, pos0, d.n_q_heads, d.n_kv_heads, hd));
+           launch_attn_bf16(s, q, layer_kv(ctx, kv, l), attn, M, pos0, d.n_q_heads, d.n_kv_heads, hd,
+                            ctx->attn_part, ctx->attn_part_floats));
     any = lora_targets({CRF_O}, tg);
     if (any) LAUNCH(ctx, s, CRF_KK_LORA_DOWN, launch_lora_down_bf16(s, attn, dq, M, dq, tg, 1, rp, u, ldu));
     {
@@ -353,7 +364,7 @@ crf_status run_layers_bf16(crf_context *ctx, const void *hb, const crf_layer_wei
       }
       p.resid = ctx->hres;
       p.ldr = D;
-      LAUNCH(ctx, s, CRF_KK_GEMM_O, launch_gemm_bf16(s, EPI_RESID, hd, p));
+      LAUNCH(ctx, s, CRF_KK_GEMM_O, gemm(EPI_RESID, p));
     }
     // MLP block
     LAUNCH(ctx, s, CRF_KK_NORM,
@@ -373,7 +384,7 @@ crf_status run_layers_bf16(crf_context *ctx, const void *hb, const crf_layer_wei
       }
       p.act = act;
       p.d_ffn = f;
-      LAUNCH(ctx, s, CRF_KK_GEMM_GATEUP, launch_gemm_bf16(s, EPI_SWIGLU, hd, p));
+      LAUNCH(ctx, s, CRF_KK_GEMM_GATEUP, gemm(EPI_SWIGLU, p));
     }
     any = lora_targets({CRF_DOWN}, tg);
     if (any) LAUNCH(ctx, s, CRF_KK_LORA_DOWN, launch_lora_down_bf16(s, act, f, M, f, tg, 1, rp, u, ldu));
@@ -388,7 +399,7 @@ crf_status run_layers_bf16(crf_context *ctx, const void *hb, const crf_layer_wei
       p.resid = ctx->hres;
       p.resid_out = (last && hout) ? (bf16 *)hout : nullptr;
       p.ldr = D;
-      LAUNCH(ctx, s, CRF_KK_GEMM_DOWN, launch_gemm_bf16(s, EPI_RESID, hd, p));
+      LAUNCH(ctx, s, CRF_KK_GEMM_DOWN, gemm(EPI_RESID, p));
     }
   }
   return CRF_OK;
@@ -492,7 +503,7 @@ crf_status crf_validate_window(const crf_model_dims *dims, int32_t l0, int32_t h
 void crf_context_destroy(crf_context *ctx) {
   if (!ctx) return;
   void *bufs[] = {ctx->hres, ctx->xn, ctx->q, ctx->attn, ctx->act, ctx->u, ctx->proj, ctx->gu, ctx->rope_cs,
-                  ctx->d_err, ctx->drift_dev};
+                  ctx->d_err, ctx->drift_dev, ctx->proj16, ctx->attn_part};
   for (void *b : bufs)
     if (b) (void)hipFree(b);
   if (ctx->drift_host) (void)hipHostFree(ctx->drift_host);
@@ -532,6 +543,10 @@ crf_status crf_context_create(const crf_model_dims *dims, int32_t max_tokens, in
   if ((st = dmalloc(ctx, &ctx->act, T * f * e)) != CRF_OK) return cleanup(st);
   if (dims->dtype == CRF_BF16) {
     if ((st = dmalloc(ctx, &ctx->u, T * 3 * ctx->rank_pad * 2)) != CRF_OK) return cleanup(st);
+    if ((st = dmalloc(ctx, &ctx->proj16, 16 * (dq + 2 * dkv) * 4)) != CRF_OK) return cleanup(st);
+    // 256 keys per split, up to 16 query rows per head: ceil(T / 256) * nq * 16 * (hd + 2)
+    ctx->attn_part_floats = (int64_t)((T + 255) / 256) * dims->n_q_heads * 16 * (dims->head_dim + 2);
+    if ((st = dmalloc(ctx, &ctx->attn_part, (size_t)ctx->attn_part_floats * 4)) != CRF_OK) return cleanup(st);
   } else {
     if ((st = dmalloc(ctx, &ctx->u, T * (size_t)(max_lora_rank > 0 ? max_lora_rank : 1) * 4)) != CRF_OK)
       return cleanup(st);
@@ -624,7 +639,7 @@ crf_status crf_decode_logits(crf_context *ctx, const crf_model_dims *dims, const
   p.resid = logits_out;
   p.ldr = vocab;
   p.resid_overwrite = 1;
-  LAUNCH(ctx, s, CRF_KK_OTHER, launch_gemm_bf16(s, EPI_RESID, d.head_dim, p));
+  LAUNCH(ctx, s, CRF_KK_OTHER, launch_gemm_skinny_bf16(s, EPI_RESID, d.head_dim, p));
   return CRF_OK;
 }
 

@@ -41,6 +41,7 @@ constexpr int BQ = 128;   // queries per workgroup
 constexpr int BKV = 64;   // keys per tile
 constexpr float RESCALE_THRESHOLD = 8.0f;  // log2 units
 constexpr int PGCAP = 2048;  // page bases staged in LDS at a time
+constexpr int KV_SPLIT = 256;  // keys per workgroup when a few query rows are split over the keys
 
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
@@ -85,7 +86,8 @@ struct PageMap {
 template <int HD, int PS>
 __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16 *__restrict__ Q, PagedKV kv,
                                                            bf16 *__restrict__ O, int Mq, int q_off, int nq,
-                                                           int nkv, uint32_t pool_bytes, int xcd_r) {
+                                                           int nkv, uint32_t pool_bytes, int xcd_r, int kv_split,
+                                                           float *__restrict__ part) {
   constexpr int CH = HD / 8;             // 16-byte chunks per row
   constexpr int KS = HD / 16;            // MFMA k-steps for S
   constexpr int HB = HD / 32;            // 32-row hd blocks of O^T
@@ -138,6 +140,13 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16 *__restric
 
   const int last_key = min(q_off + q0 + BQ, M) - 1;
   const int ntiles = last_key / BKV + 1;
+  // Split over keys (a few query rows over a long prefix): this workgroup takes
+  // tiles [t_begin, t_end) and leaves an unnormalised partial for the merge.
+  int t_begin = 0, t_end = ntiles;
+  if (kv_split > 0) {
+    t_begin = blockIdx.y * (kv_split / BKV);
+    t_end = min(ntiles, t_begin + kv_split / BKV);
+  }
   const int n_pages_needed = last_key / ps + 1;
 
   // pgbase[i] = base of logical page pg_first + i; refilled only between barriers.
@@ -208,7 +217,9 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16 *__restric
   for (int b = 0; b < HB; ++b)
 #pragma unroll
     for (int v = 0; v < 16; ++v) oacc[b][v] = 0.f;
-  float m_run = -INFINITY, l_run = 0.f;
+  // finite floor instead of -inf: a split may see no visible key for a row,
+  // and exp2(score - floor) of a masked score is still 0
+  float m_run = -1e30f, l_run = 0.f;
   const float c2 = 1.4426950408889634f / sqrtf((float)HD);  // log2(e) / sqrt(hd)
 
   // Transpose-read coordinates: 16-lane group gq covers hd 16*(gq&1) .. +15 of a
@@ -223,7 +234,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16 *__restric
     const int kt0 = it * BKV;
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
-    if (it + 1 < ntiles) {
+    if (it + 1 < t_end) {
       const int next_last_page = (min(kt0 + 2 * BKV, M) - 1) / ps;
       if (next_last_page >= pg_first + PGCAP) {
         fill_pages((kt0 + BKV) / ps);
@@ -231,7 +242,8 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16 *__restric
       }
       dma(kt0 + BKV, kn, vn);
     }
-    if (kt0 > q_off + q0w + 31) return;  // every key of this tile is in this wave's future
+    // every key of this tile is in this wave's future, or every row of the wave is padding
+    if (kt0 > q_off + q0w + 31 || q0w >= Mq) return;
     f32x16 sacc[2];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
@@ -313,16 +325,28 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16 *__restric
     }
   };
 
-  fill_pages(0);
+  fill_pages(t_begin * BKV / ps);
   __syncthreads();
-  dma(0, ks0, vs0);
-  for (int it = 0; it < ntiles; it += 2) {
+  dma(t_begin * BKV, ks0, vs0);
+  for (int it = t_begin; it < t_end; it += 2) {
     tile(it, ks0, vs0, ks1, vs1);
-    if (it + 1 < ntiles) tile(it + 1, ks1, vs1, ks0, vs0);
+    if (it + 1 < t_end) tile(it + 1, ks1, vs1, ks0, vs0);
   }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
   if (qi >= Mq) return;
+  if (kv_split > 0) {  // partial: unnormalised O^T rows, then the running max and sum
+    float *prow = part + (((int64_t)blockIdx.y * nq + head) * Mq + qi) * (HD + 2);
+#pragma unroll
+    for (int b = 0; b < HB; ++b)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) prow[b * 32 + 8 * (v / 4) + 4 * g + (v % 4)] = oacc[b][v];
+    if (g == 0) {
+      prow[HD] = m_run;
+      prow[HD + 1] = l_tot;
+    }
+    return;
+  }
   const float inv = 1.0f / l_tot;
   bf16 *orow = O + (int64_t)qi * dq + head * HD;
 #pragma unroll
@@ -335,35 +359,67 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16 *__restric
     }
 }
 
+// Merge of the key splits of one (query row, head): O = sum_s 2^(m_s - m) O_s /
+// sum_s 2^(m_s - m) l_s with m = max_s m_s (scores in log2 units).
+template <int HD>
+__global__ __launch_bounds__(64) void attn_merge_kernel(const float *__restrict__ part, bf16 *__restrict__ O,
+                                                        int Mq, int nq, int n_splits) {
+  const int qi = blockIdx.x / nq, head = blockIdx.x % nq;
+  const int64_t stride = (int64_t)nq * Mq * (HD + 2);
+  const float *p0 = part + ((int64_t)head * Mq + qi) * (HD + 2);
+  float m = -INFINITY;
+  for (int sp = 0; sp < n_splits; ++sp) m = fmaxf(m, p0[sp * stride + HD]);
+  float l = 0.f, o[HD / 64] = {};
+  for (int sp = 0; sp < n_splits; ++sp) {
+    const float *ps = p0 + sp * stride;
+    const float w = exp2f(ps[HD] - m);
+    l += w * ps[HD + 1];
+#pragma unroll
+    for (int e = 0; e < HD / 64; ++e) o[e] += w * ps[threadIdx.x + 64 * e];
+  }
+  bf16 *orow = O + (int64_t)qi * nq * HD + head * HD;
+#pragma unroll
+  for (int e = 0; e < HD / 64; ++e) orow[threadIdx.x + 64 * e] = f2bf(o[e] / l);
+}
+
 template <int HD>
 void launch(hipStream_t s, const bf16 *Q, const PagedKV &kv, bf16 *O, int Mq, int q_off, int nq, int nkv,
-            uint32_t pool_bytes) {
+            uint32_t pool_bytes, float *part, int64_t part_floats) {
   const int nqb = (Mq + BQ - 1) / BQ;
-  int xcd_r = 0, grid = nqb * nq;
-  if (nkv <= 8 && 8 % nkv == 0) {
+  int xcd_r = 0, grid = nqb * nq, n_splits = 1, kv_split = 0;
+  const int64_t keys = (int64_t)q_off + Mq;
+  if (part && Mq <= 16 && keys > 2 * KV_SPLIT) {
+    n_splits = (int)((keys + KV_SPLIT - 1) / KV_SPLIT);
+    if ((int64_t)n_splits * nq * Mq * (HD + 2) <= part_floats) kv_split = KV_SPLIT;
+    else n_splits = 1;
+  }
+  if (kv_split == 0 && nkv <= 8 && 8 % nkv == 0) {
     xcd_r = 8 / nkv;
     grid = 8 * (nq / nkv) * ((nqb + xcd_r - 1) / xcd_r);
   }
+  const dim3 g3(grid, n_splits);
   if (kv.page_size == 16)
-    hipLaunchKernelGGL((attn_bf16_kernel<HD, 16>), dim3(grid), dim3(256), 0, s, Q, kv, O, Mq, q_off, nq, nkv, pool_bytes,
-                       xcd_r);
+    hipLaunchKernelGGL((attn_bf16_kernel<HD, 16>), g3, dim3(256), 0, s, Q, kv, O, Mq, q_off, nq, nkv, pool_bytes,
+                       xcd_r, kv_split, part);
   else
-    hipLaunchKernelGGL((attn_bf16_kernel<HD, 0>), dim3(grid), dim3(256), 0, s, Q, kv, O, Mq, q_off, nq, nkv, pool_bytes,
-                       xcd_r);
+    hipLaunchKernelGGL((attn_bf16_kernel<HD, 0>), g3, dim3(256), 0, s, Q, kv, O, Mq, q_off, nq, nkv, pool_bytes,
+                       xcd_r, kv_split, part);
+  if (kv_split > 0)
+    hipLaunchKernelGGL((attn_merge_kernel<HD>), dim3(Mq * nq), dim3(64), 0, s, part, O, Mq, nq, n_splits);
 }
 
 }  // namespace
 
 hipError_t launch_attn_bf16(hipStream_t s, const bf16 *Q, const PagedKV &kv, bf16 *O, int Mq, int q_off, int nq,
-                            int nkv, int hd) {
+                            int nkv, int hd, float *part, int64_t part_floats) {
   if (Mq <= 0) return hipSuccess;
   if (q_off < 0) return hipErrorInvalidValue;
   const int64_t bytes = (int64_t)kv.n_pages * kv.page_stride * 2;
   if (bytes >= (int64_t)CRF_OOB) return hipErrorInvalidValue;
   if (hd == 128)
-    launch<128>(s, Q, kv, O, Mq, q_off, nq, nkv, (uint32_t)bytes);
+    launch<128>(s, Q, kv, O, Mq, q_off, nq, nkv, (uint32_t)bytes, part, part_floats);
   else if (hd == 64)
-    launch<64>(s, Q, kv, O, Mq, q_off, nq, nkv, (uint32_t)bytes);
+    launch<64>(s, Q, kv, O, Mq, q_off, nq, nkv, (uint32_t)bytes, part, part_floats);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

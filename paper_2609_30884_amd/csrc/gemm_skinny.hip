@@ -1,0 +1,191 @@
+// Projections of a few token rows (M <= 16: the new tokens of a decoding step,
+// or a very short window).  There the weights are streamed once and used M
+// times, so the work is HBM-bound and the 256-row tiles of gemm_bf16 would sit
+// mostly empty.  Instead, one workgroup owns 16 output features (32 for
+// gate/up: the same 16 features of both) for all M tokens: its 4 waves split K,
+// each issuing v_mfma_f32_16x16x32_bf16 with the weight rows as operand A and
+// the token rows as operand B, several k-steps of loads in flight; the partial
+// sums meet in LDS, wave 0 adds the adapter delta (U B^T, one more MFMA step
+// per 32 of rank) and runs the epilogue.  A lane ends up with 4 consecutive
+// features of one token, as in gemm_bf16:
+//   EPI_RESID  resid[m, f] (+)= acc, optional bf16 copy;
+//   EPI_SWIGLU act[m, f] = silu(gate) * up;
+//   EPI_QKV    fp32 projections to `proj`; qkv_post_bf16 then adds the bias,
+//              rotates Q and K and writes Q and the paged K/V.
+#include "kernels.hpp"
+
+namespace crf {
+namespace {
+
+constexpr int UNROLL = 8;  // k-steps of loads issued before their MFMAs
+
+// Row `r` (tile space, as in gemm_bf16) of the weight matrix and its segment.
+CRF_DEV const bf16 *skinny_weight_row(const GemmParams &p, GemmEpi epi, int r, int block, int &seg, int &local) {
+  if (epi == EPI_SWIGLU) {  // block 0: gate rows, block 1: up rows of the same features
+    seg = block;
+    local = r;
+    return p.w[block] + (int64_t)r * p.K;
+  }
+  if (epi == EPI_QKV) {
+    seg = r < p.seg1 ? 0 : (r < p.seg2 ? 1 : 2);
+    local = r - (seg == 0 ? 0 : (seg == 1 ? p.seg1 : p.seg2));
+    return p.w[seg] + (int64_t)local * p.K;
+  }
+  seg = 0;
+  local = r;
+  return p.w[0] + (int64_t)r * p.K;
+}
+
+template <int EPI, int NB>
+__global__ __launch_bounds__(256) void gemm_skinny_kernel(const GemmParams p) {
+  __shared__ f32x4 red[4][NB][64];
+  const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
+  const int f0 = blockIdx.x * 16;  // first output feature of the workgroup
+  const int nrows = EPI == EPI_SWIGLU ? p.d_ffn : p.N;
+  const int tok = min(lane % 16, p.M - 1);  // rows past M repeat the last token; never stored
+  const int kq = (lane / 16) * 8;
+  const bf16 *xrow = p.X + (int64_t)tok * p.ldx + kq;
+  const bf16 *wrow[NB];
+  int seg[NB], local[NB];
+#pragma unroll
+  for (int b = 0; b < NB; ++b)
+    wrow[b] = skinny_weight_row(p, (GemmEpi)EPI, min(f0 + lane % 16, nrows - 1), b, seg[b], local[b]) + kq;
+
+  f32x4 acc[NB];
+#pragma unroll
+  for (int b = 0; b < NB; ++b) acc[b] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int nsteps = p.K / 32;
+  int st = wave;
+  for (; st + 4 * (UNROLL - 1) < nsteps; st += 4 * UNROLL) {
+    bf16x8 xb[UNROLL], wb[UNROLL][NB];
+#pragma unroll
+    for (int u = 0; u < UNROLL; ++u) {
+      const int k = (st + 4 * u) * 32;
+      xb[u] = as_bf16x8(ld16(xrow + k));
+#pragma unroll
+      for (int b = 0; b < NB; ++b) wb[u][b] = as_bf16x8(ld16(wrow[b] + k));
+    }
+#pragma unroll
+    for (int u = 0; u < UNROLL; ++u)
+#pragma unroll
+      for (int b = 0; b < NB; ++b) acc[b] = mfma16(wb[u][b], xb[u], acc[b]);
+  }
+  for (; st < nsteps; st += 4) {
+    const int k = st * 32;
+    const bf16x8 xb = as_bf16x8(ld16(xrow + k));
+#pragma unroll
+    for (int b = 0; b < NB; ++b) acc[b] = mfma16(as_bf16x8(ld16(wrow[b] + k)), xb, acc[b]);
+  }
+#pragma unroll
+  for (int b = 0; b < NB; ++b) red[wave][b][lane] = acc[b];
+  __syncthreads();
+  if (wave != 0) return;
+#pragma unroll
+  for (int b = 0; b < NB; ++b) {
+    acc[b] = red[0][b][lane];
+#pragma unroll
+    for (int w = 1; w < 4; ++w) acc[b] += red[w][b][lane];
+  }
+  // adapter delta: acc += U[token, ucol + j] * lb[row, j], j < rank (zero-padded to 32)
+  if (p.U) {
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      const bf16 *lb = p.lb[seg[b]];
+      if (!lb) continue;
+      for (int kk = 0; kk < p.kpad; kk += 32) {
+        const int j = kk + kq;
+        u32x4 av = {0u, 0u, 0u, 0u}, uv = {0u, 0u, 0u, 0u};
+        if (j < p.rank) av = ld16(lb + (int64_t)local[b] * p.rank + j);
+        if (j < p.kpad) uv = ld16(p.U + (int64_t)tok * p.ldu + p.ucol[seg[b]] + j);
+        acc[b] = mfma16(as_bf16x8(av), as_bf16x8(uv), acc[b]);
+      }
+    }
+  }
+  const int m = lane % 16;
+  const int f = f0 + 4 * (lane / 16);  // first of this lane's 4 features
+  if (m >= p.M || f >= nrows) return;
+  if (EPI == EPI_RESID) {
+    float *rp = p.resid + (int64_t)m * p.ldr + f;
+    f32x4 r = p.resid_overwrite ? f32x4{0.f, 0.f, 0.f, 0.f} : *reinterpret_cast<f32x4 *>(rp);
+    r += acc[0];
+    *reinterpret_cast<f32x4 *>(rp) = r;
+    if (p.resid_out) st8(p.resid_out + (int64_t)m * p.ldr + f, pack_bf16x4(r[0], r[1], r[2], r[3]));
+  } else if (EPI == EPI_SWIGLU) {
+    float o[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float g = acc[0][i], u = acc[NB - 1][i];
+      o[i] = g / (1.0f + __expf(-g)) * u;
+    }
+    st8(p.act + (int64_t)m * p.d_ffn + f, pack_bf16x4(o[0], o[1], o[2], o[3]));
+  } else {
+    *reinterpret_cast<f32x4 *>(p.proj + (int64_t)m * p.N + f) = acc[0];
+  }
+}
+
+// Bias, rotation (token row m at position pos0 + m) and stores of the fp32
+// projections [M, N] (segments [0, seg1) Q, [seg1, seg2) K, [seg2, N) V; each a
+// whole number of heads).  One thread per (row, head, rotary pair).
+__global__ void qkv_post_bf16_kernel(const GemmParams p, int hd) {
+  const int half = hd / 2;
+  const int heads = p.N / hd;
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (int64_t)p.M * heads * half) return;
+  const int i = (int)(idx % half);
+  const int h = (int)((idx / half) % heads);
+  const int m = (int)(idx / ((int64_t)half * heads));
+  const int r0 = h * hd;
+  const int seg = r0 < p.seg1 ? 0 : (r0 < p.seg2 ? 1 : 2);
+  const int hl = (r0 - (seg == 0 ? 0 : (seg == 1 ? p.seg1 : p.seg2))) / hd;
+  const float *row = p.proj + (int64_t)m * p.N + r0;
+  float x1 = row[i], x2 = row[i + half];
+  if (p.bias[seg]) {
+    x1 += bf2f(p.bias[seg][hl * hd + i]);
+    x2 += bf2f(p.bias[seg][hl * hd + i + half]);
+  }
+  if (seg < 2) {
+    const float2 c = p.rope_cs[(int64_t)(p.pos0 + m) * half + i];
+    const float y1 = x1 * c.x - x2 * c.y, y2 = x2 * c.x + x1 * c.y;
+    x1 = y1;
+    x2 = y2;
+  }
+  bf16 *dst;
+  if (seg == 0) {
+    dst = p.q_out + (int64_t)m * p.dq + (int64_t)hl * hd;
+  } else {
+    const int64_t r = paged_row(p.kv, p.pos0 + m, hl, hd);
+    if (r < 0) return;
+    dst = (bf16 *)(seg == 1 ? p.kv.k : p.kv.v) + r;
+  }
+  dst[i] = f2bf(x1);
+  dst[i + half] = f2bf(x2);
+}
+
+}  // namespace
+
+hipError_t launch_gemm_skinny_bf16(hipStream_t s, GemmEpi epi, int hd, const GemmParams &p) {
+  if (p.M <= 0 || p.N <= 0) return hipSuccess;
+  if (p.M > 16 || p.K % 32 || (p.U && p.kpad % 16)) return hipErrorInvalidValue;
+  switch (epi) {
+    case EPI_RESID:
+      if (p.N % 4) return hipErrorInvalidValue;
+      hipLaunchKernelGGL((gemm_skinny_kernel<EPI_RESID, 1>), dim3((p.N + 15) / 16), dim3(256), 0, s, p);
+      break;
+    case EPI_SWIGLU:
+      if (p.d_ffn % 16) return hipErrorInvalidValue;
+      hipLaunchKernelGGL((gemm_skinny_kernel<EPI_SWIGLU, 2>), dim3(p.d_ffn / 16), dim3(256), 0, s, p);
+      break;
+    case EPI_QKV: {
+      if (!p.proj || p.N % hd || p.seg1 % hd || p.seg2 % hd) return hipErrorInvalidValue;
+      hipLaunchKernelGGL((gemm_skinny_kernel<EPI_QKV, 1>), dim3((p.N + 15) / 16), dim3(256), 0, s, p);
+      const hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
+      const int64_t n = (int64_t)p.M * (p.N / hd) * (hd / 2);
+      hipLaunchKernelGGL(qkv_post_bf16_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, p, hd);
+      break;
+    }
+  }
+  return hipGetLastError();
+}
+
+}  // namespace crf

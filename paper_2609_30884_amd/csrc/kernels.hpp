@@ -69,12 +69,18 @@ struct GemmParams {
   // EPI_SWIGLU: act[m, f] = silu(gate) * up
   bf16 *act;
   int d_ffn;
+  // EPI_QKV with few token rows: fp32 projections [M, N] before the rotary/paged stores
+  float *proj;
 };
 hipError_t launch_gemm_bf16(hipStream_t s, GemmEpi epi, int hd, const GemmParams &p);
+// The same projections for M <= 16 token rows (weight-streaming bound).
+hipError_t launch_gemm_skinny_bf16(hipStream_t s, GemmEpi epi, int hd, const GemmParams &p);
 
 // Query rows 0..Mq-1 at positions q_off..q_off+Mq-1 over keys 0..q_off+Mq-1.
+// part (nullable, part_floats floats): workspace for splitting a few query
+// rows (<= 16) over the keys of a long prefix.
 hipError_t launch_attn_bf16(hipStream_t s, const bf16 *Q, const PagedKV &kv, bf16 *O, int Mq, int q_off, int nq,
-                            int nkv, int hd);
+                            int nkv, int hd, float *part, int64_t part_floats);
 
 // ---------------------------------------------------------------- drift
 struct DriftSeg {
