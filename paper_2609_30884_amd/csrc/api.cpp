@@ -46,6 +46,8 @@ struct crf_context {
   float *proj16 = nullptr;  // bf16 path, <= 16 token rows: fp32 Q/K/V projections [16, dq + 2 dkv]
   float *attn_part = nullptr;  // bf16 path, <= 16 query rows: key-split attention partials
   int64_t attn_part_floats = 0;
+  float *lora_part = nullptr;  // bf16 path, <= 16 token rows: K-split LoRA down-projection partials
+  int64_t lora_part_floats = 0;
   // drift staging
   void *drift_host = nullptr;
   size_t drift_host_bytes = 0;
@@ -303,7 +305,7 @@ crf_status run_layers_bf16(crf_context *ctx, const void *hb, const crf_layer_wei
       // Nothing reads this layer's output: its cache entry depends only on its
       // input through the K and V projections, so only those run.
       const bool kv_any = lora_targets({CRF_K, CRF_V}, tg);
-      if (kv_any) LAUNCH(ctx, s, CRF_KK_LORA_DOWN, launch_lora_down_bf16(s, xn, D, M, D, tg, 2, rp, u, ldu));
+      if (kv_any) LAUNCH(ctx, s, CRF_KK_LORA_DOWN, launch_lora_down_bf16(s, xn, D, M, D, tg, 2, rp, u, ldu, ctx->lora_part, ctx->lora_part_floats));
       GemmParams p = base_params(xn, D, 2 * dkv);
       p.w[1] = (const bf16 *)w.w[CRF_K];
       p.w[2] = (const bf16 *)w.w[CRF_V];
@@ -325,7 +327,7 @@ crf_status run_layers_bf16(crf_context *ctx, const void *hb, const crf_layer_wei
       break;
     }
     bool any = lora_targets({CRF_Q, CRF_K, CRF_V}, tg);
-    if (any) LAUNCH(ctx, s, CRF_KK_LORA_DOWN, launch_lora_down_bf16(s, xn, D, M, D, tg, 3, rp, u, ldu));
+    if (any) LAUNCH(ctx, s, CRF_KK_LORA_DOWN, launch_lora_down_bf16(s, xn, D, M, D, tg, 3, rp, u, ldu, ctx->lora_part, ctx->lora_part_floats));
     {
       GemmParams p = base_params(xn, D, dq + 2 * dkv);
       p.w[0] = (const bf16 *)w.w[CRF_Q];
@@ -353,7 +355,7 @@ crf_status run_layers_bf16(crf_context *ctx, const void *hb, const crf_layer_wei
            launch_attn_bf16(s, q, layer_kv(ctx, kv, l), attn, M, pos0, d.n_q_heads, d.n_kv_heads, hd,
                             ctx->attn_part, ctx->attn_part_floats));
     any = lora_targets({CRF_O}, tg);
-    if (any) LAUNCH(ctx, s, CRF_KK_LORA_DOWN, launch_lora_down_bf16(s, attn, dq, M, dq, tg, 1, rp, u, ldu));
+    if (any) LAUNCH(ctx, s, CRF_KK_LORA_DOWN, launch_lora_down_bf16(s, attn, dq, M, dq, tg, 1, rp, u, ldu, ctx->lora_part, ctx->lora_part_floats));
     {
       GemmParams p = base_params(attn, dq, D);
       p.w[0] = (const bf16 *)w.w[CRF_O];
@@ -370,7 +372,7 @@ crf_status run_layers_bf16(crf_context *ctx, const void *hb, const crf_layer_wei
     LAUNCH(ctx, s, CRF_KK_NORM,
            launch_rmsnorm(s, ctx->hres, true, w.mlp_norm, false, xn, false, nullptr, M, D, d.rms_eps));
     any = lora_targets({CRF_GATE, CRF_UP}, tg);
-    if (any) LAUNCH(ctx, s, CRF_KK_LORA_DOWN, launch_lora_down_bf16(s, xn, D, M, D, tg, 2, rp, u, ldu));
+    if (any) LAUNCH(ctx, s, CRF_KK_LORA_DOWN, launch_lora_down_bf16(s, xn, D, M, D, tg, 2, rp, u, ldu, ctx->lora_part, ctx->lora_part_floats));
     {
       GemmParams p = base_params(xn, D, 2 * f);
       p.w[0] = (const bf16 *)w.w[CRF_GATE];
@@ -387,7 +389,7 @@ crf_status run_layers_bf16(crf_context *ctx, const void *hb, const crf_layer_wei
       LAUNCH(ctx, s, CRF_KK_GEMM_GATEUP, gemm(EPI_SWIGLU, p));
     }
     any = lora_targets({CRF_DOWN}, tg);
-    if (any) LAUNCH(ctx, s, CRF_KK_LORA_DOWN, launch_lora_down_bf16(s, act, f, M, f, tg, 1, rp, u, ldu));
+    if (any) LAUNCH(ctx, s, CRF_KK_LORA_DOWN, launch_lora_down_bf16(s, act, f, M, f, tg, 1, rp, u, ldu, ctx->lora_part, ctx->lora_part_floats));
     {
       GemmParams p = base_params(act, f, D);
       p.w[0] = (const bf16 *)w.w[CRF_DOWN];
@@ -503,7 +505,7 @@ crf_status crf_validate_window(const crf_model_dims *dims, int32_t l0, int32_t h
 void crf_context_destroy(crf_context *ctx) {
   if (!ctx) return;
   void *bufs[] = {ctx->hres, ctx->xn, ctx->q, ctx->attn, ctx->act, ctx->u, ctx->proj, ctx->gu, ctx->rope_cs,
-                  ctx->d_err, ctx->drift_dev, ctx->proj16, ctx->attn_part};
+                  ctx->d_err, ctx->drift_dev, ctx->proj16, ctx->attn_part, ctx->lora_part};
   for (void *b : bufs)
     if (b) (void)hipFree(b);
   if (ctx->drift_host) (void)hipHostFree(ctx->drift_host);
@@ -544,9 +546,12 @@ crf_status crf_context_create(const crf_model_dims *dims, int32_t max_tokens, in
   if (dims->dtype == CRF_BF16) {
     if ((st = dmalloc(ctx, &ctx->u, T * 3 * ctx->rank_pad * 2)) != CRF_OK) return cleanup(st);
     if ((st = dmalloc(ctx, &ctx->proj16, 16 * (dq + 2 * dkv) * 4)) != CRF_OK) return cleanup(st);
-    // 256 keys per split, up to 16 query rows per head: ceil(T / 256) * nq * 16 * (hd + 2)
-    ctx->attn_part_floats = (int64_t)((T + 255) / 256) * dims->n_q_heads * 16 * (dims->head_dim + 2);
+    // key splits of >= 64 keys, up to 16 query rows per head, rows of hd + 4 floats
+    ctx->attn_part_floats = (int64_t)((T + 63) / 64) * dims->n_q_heads * 16 * (dims->head_dim + 4);
     if ((st = dmalloc(ctx, &ctx->attn_part, (size_t)ctx->attn_part_floats * 4)) != CRF_OK) return cleanup(st);
+    // K splits of >= 256 for up to 16 rows and three targets
+    ctx->lora_part_floats = (int64_t)((std::max({D, f, dq}) + 255) / 256) * 16 * 3 * ctx->rank_pad;
+    if ((st = dmalloc(ctx, &ctx->lora_part, (size_t)ctx->lora_part_floats * 4)) != CRF_OK) return cleanup(st);
   } else {
     if ((st = dmalloc(ctx, &ctx->u, T * (size_t)(max_lora_rank > 0 ? max_lora_rank : 1) * 4)) != CRF_OK)
       return cleanup(st);

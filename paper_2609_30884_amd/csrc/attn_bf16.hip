@@ -32,6 +32,8 @@
 // side on one L2.
 #include <math.h>
 
+#include <algorithm>
+
 #include "kernels.hpp"
 
 namespace crf {
@@ -41,7 +43,7 @@ constexpr int BQ = 128;   // queries per workgroup
 constexpr int BKV = 64;   // keys per tile
 constexpr float RESCALE_THRESHOLD = 8.0f;  // log2 units
 constexpr int PGCAP = 2048;  // page bases staged in LDS at a time
-constexpr int KV_SPLIT = 256;  // keys per workgroup when a few query rows are split over the keys
+constexpr int SPLIT_WG = 1024;  // workgroups aimed at when a few query rows are split over the keys
 
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
@@ -86,8 +88,8 @@ struct PageMap {
 template <int HD, int PS>
 __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16 *__restrict__ Q, PagedKV kv,
                                                            bf16 *__restrict__ O, int Mq, int q_off, int nq,
-                                                           int nkv, uint32_t pool_bytes, int xcd_r, int kv_split,
-                                                           float *__restrict__ part) {
+                                                           int nkv, uint32_t pool_bytes, int xcd_r,
+                                                           int split_tiles, int packed, float *__restrict__ part) {
   constexpr int CH = HD / 8;             // 16-byte chunks per row
   constexpr int KS = HD / 16;            // MFMA k-steps for S
   constexpr int HB = HD / 32;            // 32-row hd blocks of O^T
@@ -106,7 +108,10 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16 *__restric
   const int nqb = (Mq + BQ - 1) / BQ;
   const int group = nq / nkv;
   int head, qblk;
-  if (xcd_r > 0) {
+  if (packed) {  // the group's query heads stacked on the rows of one tile
+    head = blockIdx.x * group;
+    qblk = 0;
+  } else if (xcd_r > 0) {
     const int x = blockIdx.x % 8, j = blockIdx.x / 8;
     const int qi = j / group;
     head = (x / xcd_r) * group + j % group;
@@ -125,12 +130,20 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16 *__restric
   const int q0w = q0 + wave * 32;
   const int qi = q0w + l32;
   const int dq = nq * HD;
+  // This lane's query: row qrow of head qhead.  Packed, tile row qi holds
+  // (query head qi / Mq of the group, query row qi % Mq).
+  const int n_rows = packed ? group * Mq : Mq;
+  const int qrow = packed ? qi % Mq : qi;
+  const int qhead = packed ? head + min(qi / Mq, group - 1) : head;
+  // first and last position of the wave's queries
+  const int pos_lo = packed ? q_off : q_off + q0w;
+  const int pos_hi = packed ? q_off + Mq - 1 : q_off + q0w + 31;
 
   bf16x8 qf[KS];
   {
-    const bf16 *qrow = Q + (int64_t)min(qi, Mq - 1) * dq + head * HD + 8 * g;
+    const bf16 *qrow_p = Q + (int64_t)min(qrow, Mq - 1) * dq + qhead * HD + 8 * g;
 #pragma unroll
-    for (int s = 0; s < KS; ++s) qf[s] = as_bf16x8(ld16(qrow + 16 * s));
+    for (int s = 0; s < KS; ++s) qf[s] = as_bf16x8(ld16(qrow_p + 16 * s));
   }
 
   const __amdgpu_buffer_rsrc_t kres = make_rsrc(kv.k, pool_bytes);
@@ -143,9 +156,9 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16 *__restric
   // Split over keys (a few query rows over a long prefix): this workgroup takes
   // tiles [t_begin, t_end) and leaves an unnormalised partial for the merge.
   int t_begin = 0, t_end = ntiles;
-  if (kv_split > 0) {
-    t_begin = blockIdx.y * (kv_split / BKV);
-    t_end = min(ntiles, t_begin + kv_split / BKV);
+  if (split_tiles > 0) {
+    t_begin = blockIdx.y * split_tiles;
+    t_end = min(ntiles, t_begin + split_tiles);
   }
   const int n_pages_needed = last_key / ps + 1;
 
@@ -243,7 +256,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16 *__restric
       dma(kt0 + BKV, kn, vn);
     }
     // every key of this tile is in this wave's future, or every row of the wave is padding
-    if (kt0 > q_off + q0w + 31 || q0w >= Mq) return;
+    if (kt0 > pos_hi || q0w >= n_rows) return;
     f32x16 sacc[2];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
@@ -269,14 +282,14 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16 *__restric
       for (int kb = 0; kb < 2; ++kb) sacc[kb] = mfma32(kf[s % 3][kb], qf[s], sacc[kb]);
       __builtin_amdgcn_sched_barrier(0);
     }
-    // causal mask (also hides keys >= M, which are always > qi for valid qi)
-    if (kt0 + BKV - 1 > q_off + q0w) {
+    // causal mask (also hides keys >= M, which are always > q_off + qrow for a valid row)
+    if (kt0 + BKV - 1 > pos_lo) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
           const int key = kt0 + kb * 32 + 8 * (v / 4) + 4 * g + (v % 4);
-          if (key > q_off + qi) sacc[kb][v] = -INFINITY;
+          if (key > q_off + qrow) sacc[kb][v] = -INFINITY;
         }
     }
     float mx = -INFINITY;
@@ -334,13 +347,15 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16 *__restric
   }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
-  if (qi >= Mq) return;
-  if (kv_split > 0) {  // partial: unnormalised O^T rows, then the running max and sum
-    float *prow = part + (((int64_t)blockIdx.y * nq + head) * Mq + qi) * (HD + 2);
+  if (qi >= n_rows) return;
+  if (split_tiles > 0) {  // partial: unnormalised O^T row, then the running max and sum
+    float *prow = part + (((int64_t)blockIdx.y * nq + qhead) * Mq + qrow) * (HD + 4);
 #pragma unroll
     for (int b = 0; b < HB; ++b)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) prow[b * 32 + 8 * (v / 4) + 4 * g + (v % 4)] = oacc[b][v];
+      for (int ii = 0; ii < 4; ++ii)
+        *reinterpret_cast<f32x4 *>(prow + b * 32 + 8 * ii + 4 * g) =
+            f32x4{oacc[b][ii * 4], oacc[b][ii * 4 + 1], oacc[b][ii * 4 + 2], oacc[b][ii * 4 + 3]};
     if (g == 0) {
       prow[HD] = m_run;
       prow[HD + 1] = l_tot;
@@ -348,7 +363,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16 *__restric
     return;
   }
   const float inv = 1.0f / l_tot;
-  bf16 *orow = O + (int64_t)qi * dq + head * HD;
+  bf16 *orow = O + (int64_t)qrow * dq + qhead * HD;
 #pragma unroll
   for (int b = 0; b < HB; ++b)
 #pragma unroll
@@ -360,52 +375,82 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16 *__restric
 }
 
 // Merge of the key splits of one (query row, head): O = sum_s 2^(m_s - m) O_s /
-// sum_s 2^(m_s - m) l_s with m = max_s m_s (scores in log2 units).
+// sum_s 2^(m_s - m) l_s with m = max_s m_s (scores in log2 units).  Groups of
+// HD / 4 threads take every NG-th split, 4 output elements per thread.
 template <int HD>
-__global__ __launch_bounds__(64) void attn_merge_kernel(const float *__restrict__ part, bf16 *__restrict__ O,
-                                                        int Mq, int nq, int n_splits) {
+__global__ __launch_bounds__(256) void attn_merge_kernel(const float *__restrict__ part, bf16 *__restrict__ O,
+                                                         int Mq, int nq, int n_splits) {
+  constexpr int TPG = HD / 4, NG = 256 / TPG;
+  __shared__ float wmax[4];
+  __shared__ f32x4 osum[NG][TPG];
+  __shared__ float lsum[NG];
   const int qi = blockIdx.x / nq, head = blockIdx.x % nq;
-  const int64_t stride = (int64_t)nq * Mq * (HD + 2);
-  const float *p0 = part + ((int64_t)head * Mq + qi) * (HD + 2);
+  const int tid = threadIdx.x;
+  const int64_t stride = (int64_t)nq * Mq * (HD + 4);
+  const float *p0 = part + ((int64_t)head * Mq + qi) * (HD + 4);
   float m = -INFINITY;
-  for (int sp = 0; sp < n_splits; ++sp) m = fmaxf(m, p0[sp * stride + HD]);
-  float l = 0.f, o[HD / 64] = {};
-  for (int sp = 0; sp < n_splits; ++sp) {
+  for (int sp = tid; sp < n_splits; sp += 256) m = fmaxf(m, p0[sp * stride + HD]);
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
+  if (tid % 64 == 0) wmax[tid / 64] = m;
+  __syncthreads();
+  m = fmaxf(fmaxf(wmax[0], wmax[1]), fmaxf(wmax[2], wmax[3]));
+  const int gi = tid / TPG, e = 4 * (tid % TPG);
+  f32x4 o = {0.f, 0.f, 0.f, 0.f};
+  float l = 0.f;
+#pragma unroll 4
+  for (int sp = gi; sp < n_splits; sp += NG) {
     const float *ps = p0 + sp * stride;
     const float w = exp2f(ps[HD] - m);
     l += w * ps[HD + 1];
-#pragma unroll
-    for (int e = 0; e < HD / 64; ++e) o[e] += w * ps[threadIdx.x + 64 * e];
+    o += w * *reinterpret_cast<const f32x4 *>(ps + e);
   }
-  bf16 *orow = O + (int64_t)qi * nq * HD + head * HD;
+  osum[gi][tid % TPG] = o;
+  if (tid % TPG == 0) lsum[gi] = l;
+  __syncthreads();
+  if (tid >= TPG) return;
+  f32x4 ot = osum[0][tid];
+  float lt = lsum[0];
 #pragma unroll
-  for (int e = 0; e < HD / 64; ++e) orow[threadIdx.x + 64 * e] = f2bf(o[e] / l);
+  for (int g2 = 1; g2 < NG; ++g2) {
+    ot += osum[g2][tid];
+    lt += lsum[g2];
+  }
+  const float inv = 1.0f / lt;
+  st8(O + (int64_t)qi * nq * HD + head * HD + e, pack_bf16x4(ot[0] * inv, ot[1] * inv, ot[2] * inv, ot[3] * inv));
 }
 
 template <int HD>
 void launch(hipStream_t s, const bf16 *Q, const PagedKV &kv, bf16 *O, int Mq, int q_off, int nq, int nkv,
             uint32_t pool_bytes, float *part, int64_t part_floats) {
   const int nqb = (Mq + BQ - 1) / BQ;
-  int xcd_r = 0, grid = nqb * nq, n_splits = 1, kv_split = 0;
+  int xcd_r = 0, grid = nqb * nq, n_splits = 1, split_tiles = 0, packed = 0;
   const int64_t keys = (int64_t)q_off + Mq;
-  if (part && Mq <= 16 && keys > 2 * KV_SPLIT) {
-    n_splits = (int)((keys + KV_SPLIT - 1) / KV_SPLIT);
-    if ((int64_t)n_splits * nq * Mq * (HD + 2) <= part_floats) kv_split = KV_SPLIT;
-    else n_splits = 1;
-  }
-  if (kv_split == 0 && nkv <= 8 && 8 % nkv == 0) {
+  const int ntiles = (int)((keys + BKV - 1) / BKV);
+  const int64_t max_splits = part ? part_floats / ((int64_t)nq * Mq * (HD + 4)) : 0;
+  if (Mq <= 16 && ntiles >= 8 && max_splits >= 2) {
+    // a few query rows over a long prefix: split the keys over workgroups;
+    // when the group's heads fit one tile, one workgroup serves all of them
+    // (the K/V tiles are read once per KV head)
+    packed = (nq / nkv) * Mq <= BQ;
+    const int units = packed ? nkv : nq;
+    split_tiles = std::max<int>(1, (ntiles * units + SPLIT_WG - 1) / SPLIT_WG);
+    split_tiles = std::max<int>(split_tiles, (int)((ntiles + max_splits - 1) / max_splits));
+    n_splits = (ntiles + split_tiles - 1) / split_tiles;
+    grid = units;
+  } else if (nkv <= 8 && 8 % nkv == 0) {
     xcd_r = 8 / nkv;
     grid = 8 * (nq / nkv) * ((nqb + xcd_r - 1) / xcd_r);
   }
   const dim3 g3(grid, n_splits);
   if (kv.page_size == 16)
     hipLaunchKernelGGL((attn_bf16_kernel<HD, 16>), g3, dim3(256), 0, s, Q, kv, O, Mq, q_off, nq, nkv, pool_bytes,
-                       xcd_r, kv_split, part);
+                       xcd_r, split_tiles, packed, part);
   else
     hipLaunchKernelGGL((attn_bf16_kernel<HD, 0>), g3, dim3(256), 0, s, Q, kv, O, Mq, q_off, nq, nkv, pool_bytes,
-                       xcd_r, kv_split, part);
-  if (kv_split > 0)
-    hipLaunchKernelGGL((attn_merge_kernel<HD>), dim3(Mq * nq), dim3(64), 0, s, part, O, Mq, nq, n_splits);
+                       xcd_r, split_tiles, packed, part);
+  if (split_tiles > 0)
+    hipLaunchKernelGGL((attn_merge_kernel<HD>), dim3(Mq * nq), dim3(256), 0, s, part, O, Mq, nq, n_splits);
 }
 
 }  // namespace

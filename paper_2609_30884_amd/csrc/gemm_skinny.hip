@@ -2,7 +2,7 @@
 // or a very short window).  There the weights are streamed once and used M
 // times, so the work is HBM-bound and the 256-row tiles of gemm_bf16 would sit
 // mostly empty.  Instead, one workgroup owns 16 output features (32 for
-// gate/up: the same 16 features of both) for all M tokens: its 4 waves split K,
+// gate/up: the same 16 features of both) for all M tokens: its 4-16 waves split K,
 // each issuing v_mfma_f32_16x16x32_bf16 with the weight rows as operand A and
 // the token rows as operand B, several k-steps of loads in flight; the partial
 // sums meet in LDS, wave 0 adds the adapter delta (U B^T, one more MFMA step
@@ -36,9 +36,9 @@ CRF_DEV const bf16 *skinny_weight_row(const GemmParams &p, GemmEpi epi, int r, i
   return p.w[0] + (int64_t)r * p.K;
 }
 
-template <int EPI, int NB>
-__global__ __launch_bounds__(256) void gemm_skinny_kernel(const GemmParams p) {
-  __shared__ f32x4 red[4][NB][64];
+template <int EPI, int NB, int W>
+__global__ __launch_bounds__(64 * W) void gemm_skinny_kernel(const GemmParams p) {
+  __shared__ f32x4 red[W][NB][64];
   const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
   const int f0 = blockIdx.x * 16;  // first output feature of the workgroup
   const int nrows = EPI == EPI_SWIGLU ? p.d_ffn : p.N;
@@ -54,27 +54,26 @@ __global__ __launch_bounds__(256) void gemm_skinny_kernel(const GemmParams p) {
   f32x4 acc[NB];
 #pragma unroll
   for (int b = 0; b < NB; ++b) acc[b] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // wave w takes k-steps w, w + W, ...; UNROLL of them are loaded before their
+  // MFMAs (the scheduling barrier keeps every load of a batch in flight at once)
   const int nsteps = p.K / 32;
-  int st = wave;
-  for (; st + 4 * (UNROLL - 1) < nsteps; st += 4 * UNROLL) {
+  for (int st = wave; st < nsteps; st += W * UNROLL) {
     bf16x8 xb[UNROLL], wb[UNROLL][NB];
 #pragma unroll
     for (int u = 0; u < UNROLL; ++u) {
-      const int k = (st + 4 * u) * 32;
-      xb[u] = as_bf16x8(ld16(xrow + k));
+      if (st + W * u < nsteps) {  // wave-uniform
+        const int k = (st + W * u) * 32;
+        xb[u] = as_bf16x8(ld16(xrow + k));
 #pragma unroll
-      for (int b = 0; b < NB; ++b) wb[u][b] = as_bf16x8(ld16(wrow[b] + k));
+        for (int b = 0; b < NB; ++b) wb[u][b] = as_bf16x8(ld16(wrow[b] + k));
+      }
     }
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int u = 0; u < UNROLL; ++u)
+      if (st + W * u < nsteps)
 #pragma unroll
-      for (int b = 0; b < NB; ++b) acc[b] = mfma16(wb[u][b], xb[u], acc[b]);
-  }
-  for (; st < nsteps; st += 4) {
-    const int k = st * 32;
-    const bf16x8 xb = as_bf16x8(ld16(xrow + k));
-#pragma unroll
-    for (int b = 0; b < NB; ++b) acc[b] = mfma16(as_bf16x8(ld16(wrow[b] + k)), xb, acc[b]);
+        for (int b = 0; b < NB; ++b) acc[b] = mfma16(wb[u][b], xb[u], acc[b]);
   }
 #pragma unroll
   for (int b = 0; b < NB; ++b) red[wave][b][lane] = acc[b];
@@ -84,7 +83,7 @@ __global__ __launch_bounds__(256) void gemm_skinny_kernel(const GemmParams p) {
   for (int b = 0; b < NB; ++b) {
     acc[b] = red[0][b][lane];
 #pragma unroll
-    for (int w = 1; w < 4; ++w) acc[b] += red[w][b][lane];
+    for (int w = 1; w < W; ++w) acc[b] += red[w][b][lane];
   }
   // adapter delta: acc += U[token, ucol + j] * lb[row, j], j < rank (zero-padded to 32)
   if (p.U) {
@@ -161,6 +160,18 @@ __global__ void qkv_post_bf16_kernel(const GemmParams p, int hd) {
   dst[i + half] = f2bf(x2);
 }
 
+// Waves per workgroup (the K split inside one workgroup): enough waves in the
+// whole grid to keep HBM busy when there are few 16-feature workgroups.
+template <int EPI, int NB>
+void launch_skinny(hipStream_t s, int n_wg, const GemmParams &p) {
+  if (n_wg >= 1024)
+    hipLaunchKernelGGL((gemm_skinny_kernel<EPI, NB, 4>), dim3(n_wg), dim3(256), 0, s, p);
+  else if (n_wg >= 512)
+    hipLaunchKernelGGL((gemm_skinny_kernel<EPI, NB, 8>), dim3(n_wg), dim3(512), 0, s, p);
+  else
+    hipLaunchKernelGGL((gemm_skinny_kernel<EPI, NB, 16>), dim3(n_wg), dim3(1024), 0, s, p);
+}
+
 }  // namespace
 
 hipError_t launch_gemm_skinny_bf16(hipStream_t s, GemmEpi epi, int hd, const GemmParams &p) {
@@ -169,15 +180,15 @@ hipError_t launch_gemm_skinny_bf16(hipStream_t s, GemmEpi epi, int hd, const Gem
   switch (epi) {
     case EPI_RESID:
       if (p.N % 4) return hipErrorInvalidValue;
-      hipLaunchKernelGGL((gemm_skinny_kernel<EPI_RESID, 1>), dim3((p.N + 15) / 16), dim3(256), 0, s, p);
+      launch_skinny<EPI_RESID, 1>(s, (p.N + 15) / 16, p);
       break;
     case EPI_SWIGLU:
       if (p.d_ffn % 16) return hipErrorInvalidValue;
-      hipLaunchKernelGGL((gemm_skinny_kernel<EPI_SWIGLU, 2>), dim3(p.d_ffn / 16), dim3(256), 0, s, p);
+      launch_skinny<EPI_SWIGLU, 2>(s, p.d_ffn / 16, p);
       break;
     case EPI_QKV: {
       if (!p.proj || p.N % hd || p.seg1 % hd || p.seg2 % hd) return hipErrorInvalidValue;
-      hipLaunchKernelGGL((gemm_skinny_kernel<EPI_QKV, 1>), dim3((p.N + 15) / 16), dim3(256), 0, s, p);
+      launch_skinny<EPI_QKV, 1>(s, (p.N + 15) / 16, p);
       const hipError_t e = hipGetLastError();
       if (e != hipSuccess) return e;
       const int64_t n = (int64_t)p.M * (p.N / hd) * (hd / 2);

@@ -36,8 +36,10 @@ struct LoraDownTarget {
 };
 // U[m, ucol_t + j] = bf16(scale_t * sum_k X[m,k] A_t[j,k]) for j < rank_pad(t)
 // (zero for rank <= j < rank_pad).
+// ws (nullable, ws_floats floats): workspace for splitting K over workgroups
+// when M <= 16.
 hipError_t launch_lora_down_bf16(hipStream_t s, const bf16 *X, int64_t ldx, int M, int K, const LoraDownTarget *t,
-                                 int n_targets, int rank_pad, bf16 *U, int ldu);
+                                 int n_targets, int rank_pad, bf16 *U, int ldu, float *ws, int64_t ws_floats);
 
 enum GemmEpi { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2 };
 

@@ -21,6 +21,8 @@ struct LdArgs {
   int n_targets, rank_pad;
   bf16 *U;
   int ldu;
+  int spw;      // k-steps of 32 per workgroup along grid.y
+  float *part;  // non-null: fp32 partial sums [grid.y][16][n_targets * rank_pad], unscaled
 };
 
 // Workgroup: 16 tokens, 4 waves splitting K (wave w takes k-steps w, w+4, ...).
@@ -47,30 +49,25 @@ __global__ __launch_bounds__(256) void lora_down_kernel(LdArgs a) {
   f32x4 acc[NB];
 #pragma unroll
   for (int b = 0; b < NB; ++b) acc[b] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const int nsteps = a.K / 32;
-  int st = wave;
-  for (; st + 4 * (UNROLL - 1) < nsteps; st += 4 * UNROLL) {
+  const int s0 = blockIdx.y * a.spw, s1 = min(a.K / 32, s0 + a.spw);
+  for (int st = s0 + wave; st < s1; st += 4 * UNROLL) {
     bf16x8 xb[UNROLL], ab[UNROLL][NB];
 #pragma unroll
     for (int u = 0; u < UNROLL; ++u) {
-      const int k = (st + 4 * u) * 32;
-      xb[u] = as_bf16x8(ld16(xrow + k));
+      if (st + 4 * u < s1) {  // wave-uniform
+        const int k = (st + 4 * u) * 32;
+        xb[u] = as_bf16x8(ld16(xrow + k));
 #pragma unroll
-      for (int b = 0; b < NB; ++b) ab[u][b] = arow[b] ? as_bf16x8(ld16(arow[b] + k)) : as_bf16x8(u32x4{0u, 0u, 0u, 0u});
+        for (int b = 0; b < NB; ++b)
+          ab[u][b] = arow[b] ? as_bf16x8(ld16(arow[b] + k)) : as_bf16x8(u32x4{0u, 0u, 0u, 0u});
+      }
     }
+    __builtin_amdgcn_sched_barrier(0);  // every load of the batch in flight before the first MFMA
 #pragma unroll
     for (int u = 0; u < UNROLL; ++u)
+      if (st + 4 * u < s1)
 #pragma unroll
-      for (int b = 0; b < NB; ++b) acc[b] = mfma16(ab[u][b], xb[u], acc[b]);
-  }
-  for (; st < nsteps; st += 4) {
-    const int k = st * 32;
-    const bf16x8 xb = as_bf16x8(ld16(xrow + k));
-#pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      const bf16x8 av = arow[b] ? as_bf16x8(ld16(arow[b] + k)) : as_bf16x8(u32x4{0u, 0u, 0u, 0u});
-      acc[b] = mfma16(av, xb, acc[b]);
-    }
+        for (int b = 0; b < NB; ++b) acc[b] = mfma16(ab[u][b], xb[u], acc[b]);
   }
 #pragma unroll
   for (int b = 0; b < NB; ++b) red[wave][b][lane] = acc[b];
@@ -83,6 +80,11 @@ __global__ __launch_bounds__(256) void lora_down_kernel(LdArgs a) {
     f32x4 v = red[0][b][lane];
 #pragma unroll
     for (int w = 1; w < 4; ++w) v += red[w][b][lane];
+    if (a.part) {  // K split over workgroups: unscaled partial, summed by lora_down_sum_kernel
+      const int ncols = a.n_targets * a.rank_pad;
+      *reinterpret_cast<f32x4 *>(a.part + ((int64_t)blockIdx.y * 16 + m) * ncols + b * 16 + (lane / 16) * 4) = v;
+      continue;
+    }
     const int t = (b * 16) / a.rank_pad;
     const int jb = b * 16 - t * a.rank_pad + (lane / 16) * 4;  // first of 4 rows held by this lane
     const float sc = a.scale[t];
@@ -90,15 +92,41 @@ __global__ __launch_bounds__(256) void lora_down_kernel(LdArgs a) {
   }
 }
 
+// U[m, ucol_t + j] = scale_t * sum over the K split of the partials (M <= 16).
+__global__ __launch_bounds__(256) void lora_down_sum_kernel(LdArgs a, int n_split) {
+  const int ncols = a.n_targets * a.rank_pad;
+  for (int i = threadIdx.x; i < a.M * ncols; i += 256) {
+    const int m = i / ncols, c = i % ncols;
+    float v = 0.f;
+    for (int y = 0; y < n_split; ++y) v += a.part[((int64_t)y * 16 + m) * ncols + c];
+    const int t = c / a.rank_pad, j = c % a.rank_pad;
+    a.U[(int64_t)m * a.ldu + a.ucol[t] + j] = f2bf(v * a.scale[t]);
+  }
+}
+
 template <int NB>
-void go(hipStream_t s, const LdArgs &a) {
-  hipLaunchKernelGGL((lora_down_kernel<NB, (NB <= 4 ? 8 : 2)>), dim3((a.M + 15) / 16), dim3(256), 0, s, a);
+void go(hipStream_t s, LdArgs a, float *ws, int64_t ws_floats) {
+  constexpr int UNROLL = NB <= 4 ? 8 : 2;
+  const int nsteps = a.K / 32;
+  // a few token rows: split K over workgroups (one batch of loads per wave)
+  // and sum the partials in a second, tiny kernel
+  const int spw = 4 * UNROLL, n_split = (nsteps + spw - 1) / spw;
+  if (a.M <= 16 && n_split > 1 && ws && (int64_t)n_split * 16 * a.n_targets * a.rank_pad <= ws_floats) {
+    a.spw = spw;
+    a.part = ws;
+    hipLaunchKernelGGL((lora_down_kernel<NB, UNROLL>), dim3(1, n_split), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(lora_down_sum_kernel, dim3(1), dim3(256), 0, s, a, n_split);
+    return;
+  }
+  a.spw = nsteps;
+  a.part = nullptr;
+  hipLaunchKernelGGL((lora_down_kernel<NB, UNROLL>), dim3((a.M + 15) / 16), dim3(256), 0, s, a);
 }
 
 }  // namespace
 
 hipError_t launch_lora_down_bf16(hipStream_t s, const bf16 *X, int64_t ldx, int M, int K, const LoraDownTarget *t,
-                                 int n_targets, int rank_pad, bf16 *U, int ldu) {
+                                 int n_targets, int rank_pad, bf16 *U, int ldu, float *ws, int64_t ws_floats) {
   if (M <= 0 || n_targets <= 0) return hipSuccess;
   if (n_targets > MAXT || n_targets * rank_pad > MAXB * 16 || rank_pad % 16 || K % 32) return hipErrorInvalidValue;
   LdArgs a{};
@@ -117,14 +145,14 @@ hipError_t launch_lora_down_bf16(hipStream_t s, const bf16 *X, int64_t ldx, int 
   a.U = U;
   a.ldu = ldu;
   switch (n_targets * rank_pad / 16) {
-    case 1: go<1>(s, a); break;
-    case 2: go<2>(s, a); break;
-    case 3: go<3>(s, a); break;
-    case 4: go<4>(s, a); break;
-    case 6: go<6>(s, a); break;
-    case 8: go<8>(s, a); break;
-    case 9: go<9>(s, a); break;
-    case 12: go<12>(s, a); break;
+    case 1: go<1>(s, a, ws, ws_floats); break;
+    case 2: go<2>(s, a, ws, ws_floats); break;
+    case 3: go<3>(s, a, ws, ws_floats); break;
+    case 4: go<4>(s, a, ws, ws_floats); break;
+    case 6: go<6>(s, a, ws, ws_floats); break;
+    case 8: go<8>(s, a, ws, ws_floats); break;
+    case 9: go<9>(s, a, ws, ws_floats); break;
+    case 12: go<12>(s, a, ws, ws_floats); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

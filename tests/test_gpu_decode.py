@@ -15,10 +15,10 @@ SMALL = dict(n_layers=4, d_model=768, n_q_heads=12, n_kv_heads=2, head_dim=64, d
 VOCAB = 1024
 
 
-def _setup(seed, n, m):
+def _setup(seed, n, m, base="qwen15b_4k", shape=SMALL, vocab=VOCAB):
     from oracle import oracle as O
     from synthetic.device import build_case, scatter_kv, to_dev
-    wl = syn.WORKLOADS["qwen15b_4k"].with_dims(**SMALL).with_window(n_tokens=n + m, l0=0, h=SMALL["n_layers"])
+    wl = syn.WORKLOADS[base].with_dims(**shape).with_window(n_tokens=n + m, l0=0, h=shape["n_layers"])
     dims = wl.dims
     N = dims.n_layers
     case = build_case(wl, seed, lora_version=3, layers=range(N))         # current adapter: version 3
@@ -30,25 +30,52 @@ def _setup(seed, n, m):
     r = syn.round_bf16
     fresh = {l: (r(k.astype(np.float32)), r(v.astype(np.float32))) for l, (k, v) in fresh.items()}
     stale = {l: (r(k.astype(np.float32)), r(v.astype(np.float32))) for l, (k, v) in stale.items()}
-    g, head = syn.gen_head(wl, seed, VOCAB)
+    g, head = syn.gen_head(wl, seed, vocab)
     dev = dict(x=to_dev(x_new, dims), g=to_dev(g, dims), head=to_dev(head, dims),
-               logits=torch.empty(VOCAB, dtype=torch.float32, device="cuda"))
+               logits=torch.empty(vocab, dtype=torch.float32, device="cuda"))
     return wl, case, x_new, fresh, stale, g, head, dev, scatter_kv
 
 
 @pytest.mark.parametrize("b", [0, 2, 4])
 def test_decode_logits_over_hybrid_cache(b):
+    _check_decode(7, 300, 3, b)
+
+
+# Longer prefixes split attention over the keys (the query heads of a KV group
+# stacked on one tile's rows when they fit, else one workgroup per query
+# head), split the LoRA down-projections over K, and run the projections with
+# 4, 8 or 16 waves per workgroup.
+SPLIT_CASES = {
+    # 16 rows x 6 heads stacked; the last key split starts after the first 4
+    # rows' positions (1020..1023), so those rows see no key in it
+    "stacked_hd64": ("qwen7b_16k", dict(n_layers=2, d_model=1536, n_q_heads=12, n_kv_heads=2, head_dim=64,
+                                        d_ffn=2048), 1020, 16, 1024),
+    # one row, hd 128; gate/up on 8 waves, LM head on 4
+    "one_row_hd128": ("qwen7b_16k", dict(n_layers=2, d_model=1024, n_q_heads=8, n_kv_heads=2, head_dim=128,
+                                         d_ffn=8192), 700, 1, 16384),
+    # 16 rows x 12 heads do not fit one tile: one workgroup per query head
+    "per_head_hd128": ("qwen15b_4k", dict(n_layers=2, d_model=1536, n_q_heads=12, n_kv_heads=1, head_dim=128,
+                                          d_ffn=2048), 600, 16, 1024),
+}
+
+
+@pytest.mark.parametrize("name", list(SPLIT_CASES))
+def test_decode_key_split_shapes(name):
+    base, shape, n, m, vocab = SPLIT_CASES[name]
+    _check_decode(11, n, m, 1, base=base, shape=shape, vocab=vocab)
+
+
+def _check_decode(seed, n, m, b, **kw):
     import paper_2609_30884_amd as crf
     from oracle import oracle as O
     from synthetic.device import gather_kv
-    seed, n, m = 7, 300, 3
-    wl, case, x_new, fresh, stale, g, head, dev, scatter_kv = _setup(seed, n, m)
+    wl, case, x_new, fresh, stale, g, head, dev, scatter_kv = _setup(seed, n, m, **kw)
     dims, N = wl.dims, wl.dims.n_layers
     hyb = O.hybrid_caches(fresh, stale, b, N)
     for l in range(N):
         scatter_kv(case.k_pool, l, case.block_table, wl.page_size, hyb[l][0])
         scatter_kv(case.v_pool, l, case.block_table, wl.page_size, hyb[l][1])
-    print(f"[case] decode n={n} m={m} boundary b={b}", flush=True)
+    print(f"[case] decode n={n} m={m} boundary b={b} dims={dims}", flush=True)
     cd = cdims(dims)
     ctx = crf.Context(cd, n + m, wl.lora_rank)
     kv = crf.kv_cache(case.k_pool, case.v_pool, case.block_table_dev, n, wl.page_size)
