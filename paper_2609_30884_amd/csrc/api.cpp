@@ -48,6 +48,9 @@ struct crf_context {
   int64_t attn_part_floats = 0;
   float *lora_part = nullptr;  // bf16 path, <= 16 token rows: K-split LoRA down-projection partials
   int64_t lora_part_floats = 0;
+  float *gemm_part = nullptr;  // bf16 path: K-part partials of the last residual GEMM tiles
+  int64_t gemm_part_floats = 0;
+  int n_cu = 0;
   // drift staging
   void *drift_host = nullptr;
   size_t drift_host_bytes = 0;
@@ -286,6 +289,9 @@ crf_status run_layers_bf16(crf_context *ctx, const void *hb, const crf_layer_wei
       p.rank = rank;
       p.rope_cs = ctx->rope_cs;
       p.pos0 = pos0;
+      p.split_part = ctx->gemm_part;
+      p.split_cap = ctx->gemm_part_floats;
+      p.n_cu = ctx->n_cu;
       return p;
     };
     LoraDownTarget tg[3];
@@ -505,7 +511,7 @@ crf_status crf_validate_window(const crf_model_dims *dims, int32_t l0, int32_t h
 void crf_context_destroy(crf_context *ctx) {
   if (!ctx) return;
   void *bufs[] = {ctx->hres, ctx->xn, ctx->q, ctx->attn, ctx->act, ctx->u, ctx->proj, ctx->gu, ctx->rope_cs,
-                  ctx->d_err, ctx->drift_dev, ctx->proj16, ctx->attn_part, ctx->lora_part};
+                  ctx->d_err, ctx->drift_dev, ctx->proj16, ctx->attn_part, ctx->lora_part, ctx->gemm_part};
   for (void *b : bufs)
     if (b) (void)hipFree(b);
   if (ctx->drift_host) (void)hipHostFree(ctx->drift_host);
@@ -552,6 +558,13 @@ crf_status crf_context_create(const crf_model_dims *dims, int32_t max_tokens, in
     // K splits of >= 256 for up to 16 rows and three targets
     ctx->lora_part_floats = (int64_t)((std::max({D, f, dq}) + 255) / 256) * 16 * 3 * ctx->rank_pad;
     if ((st = dmalloc(ctx, &ctx->lora_part, (size_t)ctx->lora_part_floats * 4)) != CRF_OK) return cleanup(st);
+    // at most one 256x256 fp32 partial per compute unit
+    if (hipDeviceGetAttribute(&ctx->n_cu, hipDeviceAttributeMultiprocessorCount, ctx->device) != hipSuccess)
+      ctx->n_cu = 0;
+    ctx->gemm_part_floats = (int64_t)std::max(ctx->n_cu, 0) * 256 * 256;
+    if (ctx->gemm_part_floats > 0 &&
+        (st = dmalloc(ctx, &ctx->gemm_part, (size_t)ctx->gemm_part_floats * 4)) != CRF_OK)
+      return cleanup(st);
   } else {
     if ((st = dmalloc(ctx, &ctx->u, T * (size_t)(max_lora_rank > 0 ? max_lora_rank : 1) * 4)) != CRF_OK)
       return cleanup(st);

@@ -21,6 +21,7 @@
 // token, which makes every epilogue lane-local (a rotary pair (f, f+hd/2) and a
 // gate/up pair live in the same lane).  16-byte LDS chunks are XOR-swizzled by
 // (row/2) mod 8 so the fragment reads are bank-conflict free.
+#include <algorithm>
 #include <type_traits>
 
 #include "kernels.hpp"
@@ -87,6 +88,15 @@ CRF_DEV int segment_of(const GemmParams &p, int r, int &local) {
   return (r >> 6) & 1;
 }
 
+// Tile t of the grouped order (GROUP_M token tiles share a weight panel).
+CRF_DEV void tile_coords(int t, int tiles_m, int tiles_n, int &tm, int &tn) {
+  const int group = GROUP_M * tiles_n;
+  const int first_m = (t / group) * GROUP_M;
+  const int gm = min(tiles_m - first_m, GROUP_M);
+  tm = first_m + (t % group) % gm;
+  tn = (t % group) / gm;
+}
+
 // WAVES = 4: 2 (features) x 2 (tokens) waves of 128 x 128.
 // WAVES = 8: 2 (features) x 4 (tokens) waves of 128 x 64.
 template <int EPI, int HD, int WAVES>
@@ -103,12 +113,25 @@ __global__ __launch_bounds__(64 * WAVES, 1) void gemm_bf16_kernel(const GemmPara
 
   const int tiles_m = (p.M + BM - 1) / BM;
   const int tiles_n = (p.N + BN - 1) / BN;
-  const int t = xcd_remap(blockIdx.x, gridDim.x);
-  const int group = GROUP_M * tiles_n;
-  const int first_m = (t / group) * GROUP_M;
-  const int gm = min(tiles_m - first_m, GROUP_M);
-  const int tm = first_m + (t % group) % gm;
-  const int tn = (t % group) / gm;
+  const int nk = p.K / BK;
+  // work item: a whole tile, or K-part `part` of one of the last tiles.  The
+  // whole tiles come first in dispatch order and the K-parts after them, each
+  // range remapped on its own so that every XCD gets an equal, contiguous
+  // share of both.
+  int w, t, part = -1, kb = 0, ke = nk;
+  if (EPI == EPI_RESID && p.split_s > 1 && (int)blockIdx.x >= p.split_first) {
+    const int n_parts = (int)gridDim.x - p.split_first;
+    w = p.split_first + xcd_remap((int)blockIdx.x - p.split_first, n_parts);
+    t = p.split_first + (w - p.split_first) / p.split_s;
+    part = (w - p.split_first) % p.split_s;
+    kb = part * nk / p.split_s;
+    ke = (part + 1) * nk / p.split_s;
+  } else {
+    w = xcd_remap(blockIdx.x, EPI == EPI_RESID && p.split_s > 1 ? p.split_first : gridDim.x);
+    t = w;
+  }
+  int tm, tn;
+  tile_coords(t, tiles_m, tiles_n, tm, tn);
   const int m0 = tm * BM, n0 = tn * BN;
 
   const int tid = threadIdx.x, lane = tid % 64;
@@ -150,6 +173,18 @@ __global__ __launch_bounds__(64 * WAVES, 1) void gemm_bf16_kernel(const GemmPara
       dma16(wres[j], dw + blk * 1024, woff[j], (uint32_t)k0 * 2);
     }
   };
+  // blocks [J0, J1) of both operands
+  auto dma_part = [&](int k0, int stage, auto j0, auto j1) {
+    constexpr int J0 = decltype(j0)::value, J1 = decltype(j1)::value;
+    lds_char *dx = (lds_char *)(lds_x + stage * BM * BK);
+    lds_char *dw = (lds_char *)(lds_w + stage * BN * BK);
+#pragma unroll
+    for (int j = J0; j < J1; ++j) {
+      const int blk = WAVES * j + wave;
+      dma16(xres, dx + blk * 1024, xoff[j], (uint32_t)k0 * 2);
+      dma16(wres[j], dw + blk * 1024, woff[j], (uint32_t)k0 * 2);
+    }
+  };
 
   f32x16 acc[4][NJ];
 #pragma unroll
@@ -159,8 +194,8 @@ __global__ __launch_bounds__(64 * WAVES, 1) void gemm_bf16_kernel(const GemmPara
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-  // ---- low-rank delta: acc += U[token, ucol_s + k] * lb_s[feature, k]
-  if (p.U) {
+  // ---- low-rank delta: acc += U[token, ucol_s + k] * lb_s[feature, k] (K-part 0 only)
+  if (p.U && part <= 0) {
     int seg[4], frow[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -190,7 +225,9 @@ __global__ __launch_bounds__(64 * WAVES, 1) void gemm_bf16_kernel(const GemmPara
     }
   }
 
-  const int nk = p.K / BK;
+  constexpr int KSTEPS = BK / 16;
+  constexpr int NMM = 4 * NJ, NDS = 4 + NJ;
+  constexpr int NMM4 = NMM;
   auto frag = [&](int stage, int s, bf16x8 (&fa)[4], bf16x8 (&fb)[NJ]) {
     const bf16 *sx = lds_x + stage * BM * BK;
     const bf16 *sw = lds_w + stage * BN * BK;
@@ -205,6 +242,60 @@ __global__ __launch_bounds__(64 * WAVES, 1) void gemm_bf16_kernel(const GemmPara
 #pragma unroll
       for (int j = 0; j < NJ; ++j) acc[i][j] = mfma32(fa[i], fb[j], acc[i][j]);
   };
+  if constexpr (WAVES == 4) {
+    // One wave per SIMD: no second wave covers a stall, so fragments are read
+    // two k-steps ahead of their MFMAs (one register set per k-step of a
+    // slice).  The slice barrier sits after k-step 1: by then this wave has
+    // read all of slice kt (its k-steps 2 and 3 were read during k-steps 0
+    // and 1), so the stage can take slice kt+2, and slice kt+1 (issued one
+    // slice earlier) has landed for the reads made during k-steps 2 and 3.
+    static_assert(BK == 64 && STAGES == 2, "two stages of 64-wide slices");
+    bf16x8 fa[4][4], fb[4][NJ];
+    // per k-step region: 16 MFMAs; the first 8 each followed by one LDS read
+    // and, when refilling, one global->LDS load
+    auto sched = [&](auto n_vmem) {
+      constexpr int NV = decltype(n_vmem)::value;
+#pragma unroll
+      for (int i = 0; i < NMM4; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        if (i < 4 + NJ) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        if (i < NV) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+      }
+    };
+    dma(kb * BK, 0);
+    dma(min(kb + 1, ke - 1) * BK, 1);
+    wait_vm<DMA_PER_SLICE>();
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    frag(0, 0, fa[0], fb[0]);
+    frag(0, 1, fa[1], fb[1]);
+    for (int kt = kb; kt < ke; ++kt) {
+      const int st = (kt - kb) & 1;
+      __builtin_amdgcn_sched_barrier(0);
+      frag(st, 2, fa[2], fb[2]);
+      mm(fa[0], fb[0]);
+      sched(std::integral_constant<int, 0>());
+      __builtin_amdgcn_sched_barrier(0);
+      frag(st, 3, fa[3], fb[3]);
+      mm(fa[1], fb[1]);
+      sched(std::integral_constant<int, 0>());
+      __builtin_amdgcn_sched_barrier(0);
+      wait_vm<0>();
+      asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+      __builtin_amdgcn_sched_barrier(0);
+      const int kn = min(kt + 2, ke - 1) * BK;  // clamped: every slice issues the same loads
+      dma_part(kn, st, std::integral_constant<int, 0>(), std::integral_constant<int, BLK / 2>());
+      frag(st ^ 1, 0, fa[0], fb[0]);
+      mm(fa[2], fb[2]);
+      sched(std::integral_constant<int, BLK>());
+      __builtin_amdgcn_sched_barrier(0);
+      dma_part(kn, st, std::integral_constant<int, BLK / 2>(), std::integral_constant<int, BLK>());
+      frag(st ^ 1, 1, fa[1], fb[1]);
+      mm(fa[3], fb[3]);
+      sched(std::integral_constant<int, BLK>());
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    wait_vm<0>();
+  } else {
   // Ring of STAGES slices.  The prologue puts slices 0..STAGES-1 in flight.
   // Each k-step is one scheduling region: its MFMAs with the next step's
   // fragment reads interleaved one by one (the MFMAs use fragments read one
@@ -214,8 +305,7 @@ __global__ __launch_bounds__(64 * WAVES, 1) void gemm_bf16_kernel(const GemmPara
   // slice kt, then the refill of that stage with slice kt+STAGES (clamped to
   // the last slice near the end, so every slice issues the same number of
   // loads), interleaved with the MFMAs and with slice kt+1's first reads.
-  constexpr int KSTEPS = BK / 16;
-  constexpr int NMM = 4 * NJ, NDS = 4 + NJ;
+
   auto interleave = [&](auto n_vmem) {
     constexpr int NV = decltype(n_vmem)::value;
 #pragma unroll
@@ -226,13 +316,13 @@ __global__ __launch_bounds__(64 * WAVES, 1) void gemm_bf16_kernel(const GemmPara
     }
   };
 #pragma unroll
-  for (int s = 0; s < STAGES; ++s) dma(min(s, nk - 1) * BK, s);
+  for (int s = 0; s < STAGES; ++s) dma(min(kb + s, ke - 1) * BK, s);
   wait_vm<(STAGES - 1) * DMA_PER_SLICE>();
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
   bf16x8 a0[4], b0[NJ], a1[4], b1[NJ];
   frag(0, 0, a0, b0);
   int st = 0;
-  for (int kt = 0; kt < nk; ++kt) {
+  for (int kt = kb; kt < ke; ++kt) {
     const int nst = st + 1 == STAGES ? 0 : st + 1;
 #pragma unroll
     for (int s = 0; s + 1 < KSTEPS; ++s) {
@@ -252,7 +342,7 @@ __global__ __launch_bounds__(64 * WAVES, 1) void gemm_bf16_kernel(const GemmPara
     wait_vm<(STAGES - 2) * DMA_PER_SLICE>();
     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
     __builtin_amdgcn_sched_barrier(0);
-    dma(min(kt + STAGES, nk - 1) * BK, st);
+    dma(min(kt + STAGES, ke - 1) * BK, st);
     frag(nst, 0, a0, b0);
     mm(a1, b1);  // KSTEPS is even: the last k-step of a slice uses (a1, b1)
     interleave(std::integral_constant<int, DMA_PER_SLICE>());
@@ -260,9 +350,24 @@ __global__ __launch_bounds__(64 * WAVES, 1) void gemm_bf16_kernel(const GemmPara
     st = nst;
   }
   wait_vm<0>();  // the clamped refills of the last slices
+  }
 
   // ---- epilogues
-  if (EPI == EPI_RESID) {
+  if (EPI == EPI_RESID && part >= 0) {  // fp32 partial of a K-part, [256 tokens][256 features]
+    float *pp = p.split_part + (int64_t)(w - p.split_first) * BM * BN;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const int ml = wm * WTM + 32 * j + l32;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int ii = 0; ii < 4; ++ii) {
+          const int nl = wn * 128 + 32 * i + 8 * ii + 4 * g;
+          *reinterpret_cast<f32x4 *>(pp + ml * BN + nl) =
+              f32x4{acc[i][j][ii * 4], acc[i][j][ii * 4 + 1], acc[i][j][ii * 4 + 2], acc[i][j][ii * 4 + 3]};
+        }
+    }
+  } else if (EPI == EPI_RESID) {
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
       const int m = m0 + wm * WTM + 32 * j + l32;
@@ -364,9 +469,53 @@ __global__ __launch_bounds__(64 * WAVES, 1) void gemm_bf16_kernel(const GemmPara
   }
 }
 
+// resid[m, n] (+)= sum over the K-parts of a split tile, in part order; one
+// thread per 4 features.
+__global__ __launch_bounds__(256) void split_reduce_kernel(const GemmParams p) {
+  const int tiles_m = (p.M + BM - 1) / BM, tiles_n = (p.N + BN - 1) / BN;
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;  // over split tiles x 256 x 64
+  const int ti = (int)(idx / (BM * BN / 4));
+  const int e = (int)(idx % (BM * BN / 4));
+  const int ml = e / (BN / 4), nl = 4 * (e % (BN / 4));
+  int tm, tn;
+  tile_coords(p.split_first + ti, tiles_m, tiles_n, tm, tn);
+  const int m = tm * BM + ml, n = tn * BN + nl;
+  if (m >= p.M || n >= p.N) return;
+  const float *pp = p.split_part + (int64_t)ti * p.split_s * BM * BN + ml * BN + nl;
+  f32x4 v = *reinterpret_cast<const f32x4 *>(pp);
+  for (int sp = 1; sp < p.split_s; ++sp) v += *reinterpret_cast<const f32x4 *>(pp + (int64_t)sp * BM * BN);
+  float *rp = p.resid + (int64_t)m * p.ldr + n;
+  f32x4 r = p.resid_overwrite ? f32x4{0.f, 0.f, 0.f, 0.f} : *reinterpret_cast<f32x4 *>(rp);
+  r += v;
+  *reinterpret_cast<f32x4 *>(rp) = r;
+  if (p.resid_out) st8(p.resid_out + (int64_t)m * p.ldr + n, pack_bf16x4(r[0], r[1], r[2], r[3]));
+}
+
 template <int EPI, int HD, int WAVES>
-hipError_t go(hipStream_t s, const GemmParams &p) {
-  const int tiles = ((p.M + BM - 1) / BM) * ((p.N + BN - 1) / BN);
+hipError_t go(hipStream_t s, const GemmParams &p0) {
+  const int tiles = ((p0.M + BM - 1) / BM) * ((p0.N + BN - 1) / BN);
+  GemmParams p = p0;
+  p.split_first = tiles;
+  p.split_s = 1;
+  if (EPI == EPI_RESID && p.split_part && p.n_cu > 0) {
+    // a last wave at most half full: split its tiles (or all tiles, when there
+    // are fewer than compute units) into K-parts of at least 8 slices
+    const int nk = p.K / BK, r = tiles % p.n_cu;
+    int first = tiles, sp = 1;
+    if (tiles < p.n_cu) {
+      first = 0;
+      sp = p.n_cu / tiles;
+    } else if (r > 0 && 2 * r <= p.n_cu) {
+      first = tiles - r;
+      sp = 2;
+    }
+    sp = std::min(sp, std::min(8, nk / 8));
+    if (sp >= 2 && (int64_t)(tiles - first) * sp * BM * BN <= p.split_cap) {
+      p.split_first = first;
+      p.split_s = sp;
+    }
+  }
+  const int grid = p.split_first + (tiles - p.split_first) * p.split_s;
   const size_t lds = (size_t)STAGES * (BM + BN) * BK * sizeof(bf16);
   static bool attr_set = false;
   if (!attr_set) {
@@ -375,7 +524,13 @@ hipError_t go(hipStream_t s, const GemmParams &p) {
     if (e != hipSuccess) return e;
     attr_set = true;
   }
-  hipLaunchKernelGGL((gemm_bf16_kernel<EPI, HD, WAVES>), dim3(tiles), dim3(64 * WAVES), lds, s, p);
+  hipLaunchKernelGGL((gemm_bf16_kernel<EPI, HD, WAVES>), dim3(grid), dim3(64 * WAVES), lds, s, p);
+  if (p.split_s > 1) {
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int64_t n = (int64_t)(tiles - p.split_first) * BM * BN / 4;
+    hipLaunchKernelGGL(split_reduce_kernel, dim3((unsigned)(n / 256)), dim3(256), 0, s, p);
+  }
   return hipGetLastError();
 }
 

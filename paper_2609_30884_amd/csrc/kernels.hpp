@@ -73,6 +73,15 @@ struct GemmParams {
   int d_ffn;
   // EPI_QKV with few token rows: fp32 projections [M, N] before the rotary/paged stores
   float *proj;
+  // EPI_RESID: when the tiles leave the last wave of the grid at most half
+  // full (n_cu compute units), the last tiles are split into K-parts that
+  // write fp32 partials to split_part (split_cap floats) and a second kernel
+  // adds them to the residual in a fixed order.  split_first / split_s are
+  // set by the launcher.
+  float *split_part;
+  int64_t split_cap;
+  int n_cu;
+  int split_first, split_s;
 };
 hipError_t launch_gemm_bf16(hipStream_t s, GemmEpi epi, int hd, const GemmParams &p);
 // The same projections for M <= 16 token rows (weight-streaming bound).
