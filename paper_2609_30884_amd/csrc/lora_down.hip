@@ -25,19 +25,22 @@ struct LdArgs {
   float *part;  // non-null: fp32 partial sums [grid.y][16][n_targets * rank_pad], unscaled
 };
 
-// Workgroup: 16 tokens, 4 waves splitting K (wave w takes k-steps w, w+4, ...).
-// Per k-step of 32: D[j, token] += A_t[j, k..k+32] . X[token, k..k+32] on the
-// 16x16x32 MFMA, one MFMA per 16-row block of the concatenated factors.  The
-// loads of UNROLL k-steps are issued before their MFMAs so enough bytes are in
-// flight to keep HBM busy; the factors (a few hundred KB) stay in L2.
-template <int NB, int UNROLL>
+// Workgroup: TB blocks of 16 tokens, 4 waves splitting K (wave w takes k-steps
+// w, w+4, ...).  Per k-step of 32: D[j, token] += A_t[j, k..k+32] .
+// X[token, k..k+32] on the 16x16x32 MFMA, one MFMA per (16-row block of the
+// concatenated factors, token block): the factors are read once per TB*16
+// tokens.  The loads of UNROLL k-steps are issued before their MFMAs so enough
+// bytes are in flight to keep HBM busy; the factors (a few hundred KB) stay in
+// L2.
+template <int NB, int UNROLL, int TB>
 __global__ __launch_bounds__(256) void lora_down_kernel(LdArgs a) {
-  __shared__ f32x4 red[4][NB][64];
+  __shared__ f32x4 red[4][NB * TB][64];
   const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
-  const int m0 = blockIdx.x * 16;
-  const int tok = min(m0 + lane % 16, a.M - 1);
+  const int m0 = blockIdx.x * 16 * TB;
   const int kq = (lane / 16) * 8;
-  const bf16 *xrow = a.X + (int64_t)tok * a.ldx + kq;
+  const bf16 *xrow[TB];
+#pragma unroll
+  for (int tb = 0; tb < TB; ++tb) xrow[tb] = a.X + (int64_t)min(m0 + 16 * tb + lane % 16, a.M - 1) * a.ldx + kq;
   // per block: factor row pointer (or null -> zeros)
   const bf16 *arow[NB];
 #pragma unroll
@@ -46,17 +49,20 @@ __global__ __launch_bounds__(256) void lora_down_kernel(LdArgs a) {
     const int j = b * 16 - t * a.rank_pad + lane % 16;
     arow[b] = (a.A[t] && j < a.rank[t]) ? a.A[t] + (int64_t)j * a.K + kq : nullptr;
   }
-  f32x4 acc[NB];
+  f32x4 acc[NB][TB];
 #pragma unroll
-  for (int b = 0; b < NB; ++b) acc[b] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int b = 0; b < NB; ++b)
+#pragma unroll
+    for (int tb = 0; tb < TB; ++tb) acc[b][tb] = f32x4{0.f, 0.f, 0.f, 0.f};
   const int s0 = blockIdx.y * a.spw, s1 = min(a.K / 32, s0 + a.spw);
   for (int st = s0 + wave; st < s1; st += 4 * UNROLL) {
-    bf16x8 xb[UNROLL], ab[UNROLL][NB];
+    bf16x8 xb[UNROLL][TB], ab[UNROLL][NB];
 #pragma unroll
     for (int u = 0; u < UNROLL; ++u) {
       if (st + 4 * u < s1) {  // wave-uniform
         const int k = (st + 4 * u) * 32;
-        xb[u] = as_bf16x8(ld16(xrow + k));
+#pragma unroll
+        for (int tb = 0; tb < TB; ++tb) xb[u][tb] = as_bf16x8(ld16(xrow[tb] + k));
 #pragma unroll
         for (int b = 0; b < NB; ++b)
           ab[u][b] = arow[b] ? as_bf16x8(ld16(arow[b] + k)) : as_bf16x8(u32x4{0u, 0u, 0u, 0u});
@@ -67,19 +73,24 @@ __global__ __launch_bounds__(256) void lora_down_kernel(LdArgs a) {
     for (int u = 0; u < UNROLL; ++u)
       if (st + 4 * u < s1)
 #pragma unroll
-        for (int b = 0; b < NB; ++b) acc[b] = mfma16(ab[u][b], xb[u], acc[b]);
+        for (int b = 0; b < NB; ++b)
+#pragma unroll
+          for (int tb = 0; tb < TB; ++tb) acc[b][tb] = mfma16(ab[u][b], xb[u][tb], acc[b][tb]);
   }
 #pragma unroll
-  for (int b = 0; b < NB; ++b) red[wave][b][lane] = acc[b];
+  for (int b = 0; b < NB; ++b)
+#pragma unroll
+    for (int tb = 0; tb < TB; ++tb) red[wave][b * TB + tb][lane] = acc[b][tb];
   __syncthreads();
-  if (wave != 0) return;
-  const int m = m0 + lane % 16;
+  // wave w finishes token block w (TB <= 4)
+  if (wave >= TB) return;
+  const int m = m0 + 16 * wave + lane % 16;
   if (m >= a.M) return;
 #pragma unroll
   for (int b = 0; b < NB; ++b) {
-    f32x4 v = red[0][b][lane];
+    f32x4 v = red[0][b * TB + wave][lane];
 #pragma unroll
-    for (int w = 1; w < 4; ++w) v += red[w][b][lane];
+    for (int w = 1; w < 4; ++w) v += red[w][b * TB + wave][lane];
     if (a.part) {  // K split over workgroups: unscaled partial, summed by lora_down_sum_kernel
       const int ncols = a.n_targets * a.rank_pad;
       *reinterpret_cast<f32x4 *>(a.part + ((int64_t)blockIdx.y * 16 + m) * ncols + b * 16 + (lane / 16) * 4) = v;
@@ -114,13 +125,19 @@ void go(hipStream_t s, LdArgs a, float *ws, int64_t ws_floats) {
   if (a.M <= 16 && n_split > 1 && ws && (int64_t)n_split * 16 * a.n_targets * a.rank_pad <= ws_floats) {
     a.spw = spw;
     a.part = ws;
-    hipLaunchKernelGGL((lora_down_kernel<NB, UNROLL>), dim3(1, n_split), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((lora_down_kernel<NB, UNROLL, 1>), dim3(1, n_split), dim3(256), 0, s, a);
     hipLaunchKernelGGL(lora_down_sum_kernel, dim3(1), dim3(256), 0, s, a, n_split);
     return;
   }
   a.spw = nsteps;
   a.part = nullptr;
-  hipLaunchKernelGGL((lora_down_kernel<NB, UNROLL>), dim3((a.M + 15) / 16), dim3(256), 0, s, a);
+  if constexpr (NB <= 4) {
+    if (a.M >= 8192) {  // 64 tokens per workgroup: the factors are read once per 64 tokens
+      hipLaunchKernelGGL((lora_down_kernel<NB, 4, 4>), dim3((a.M + 63) / 64), dim3(256), 0, s, a);
+      return;
+    }
+  }
+  hipLaunchKernelGGL((lora_down_kernel<NB, UNROLL, 1>), dim3((a.M + 15) / 16), dim3(256), 0, s, a);
 }
 
 }  // namespace

@@ -92,15 +92,18 @@ def test_prefix_longer_than_workspace_is_rejected():
     assert bool(canary_mask(case.k_pool).all()), "nothing may run when the request is rejected"
 
 
-@pytest.mark.parametrize("dims,n", [
-    (dict(n_layers=4, d_model=768, n_q_heads=12, n_kv_heads=2, head_dim=64, d_ffn=2048), 5500),
-    (dict(n_layers=4, d_model=768, n_q_heads=24, n_kv_heads=4, head_dim=128, d_ffn=1024), 2800),
+@pytest.mark.parametrize("base,dims,n", [
+    ("qwen15b_4k", dict(n_layers=4, d_model=768, n_q_heads=12, n_kv_heads=2, head_dim=64, d_ffn=2048), 5500),
+    ("qwen15b_4k", dict(n_layers=4, d_model=768, n_q_heads=24, n_kv_heads=4, head_dim=128, d_ffn=1024), 2800),
+    # adapters on all seven projections over 8200 tokens: the LoRA down-projections
+    # take 64 tokens per workgroup (8 tokens in the last one)
+    ("qwen7b_16k", dict(n_layers=4, d_model=256, n_q_heads=2, n_kv_heads=1, head_dim=128, d_ffn=512), 8200),
 ])
-def test_bf16_longer_prefixes(dims, n):
+def test_bf16_longer_prefixes(base, dims, n):
     """Longer ragged prefixes (dozens of query blocks per head, more query
     heads than model width) with head_dim 64 and 128."""
     from synthetic.device import build_case
-    wl = syn.WORKLOADS["qwen15b_4k"].with_dims(**dims).with_window(n_tokens=n, l0=1, h=2)
+    wl = syn.WORKLOADS[base].with_dims(**dims).with_window(n_tokens=n, l0=1, h=2)
     print(f"[case] longer prefix {dims} n={n}", flush=True)
     case = build_case(wl, 29)
     run_gpu_window(case)
