@@ -104,15 +104,22 @@ __global__ __launch_bounds__(256) void lora_down_kernel(LdArgs a) {
 }
 
 // U[m, ucol_t + j] = scale_t * sum over the K split of the partials (M <= 16).
+// 16 lanes per output, lane l adding the parts l, l + 16, ...; the 16 sums are
+// then combined in a fixed order.
 __global__ __launch_bounds__(256) void lora_down_sum_kernel(LdArgs a, int n_split) {
   const int ncols = a.n_targets * a.rank_pad;
-  for (int i = threadIdx.x; i < a.M * ncols; i += 256) {
-    const int m = i / ncols, c = i % ncols;
-    float v = 0.f;
-    for (int y = 0; y < n_split; ++y) v += a.part[((int64_t)y * 16 + m) * ncols + c];
-    const int t = c / a.rank_pad, j = c % a.rank_pad;
-    a.U[(int64_t)m * a.ldu + a.ucol[t] + j] = f2bf(v * a.scale[t]);
+  const int o = blockIdx.x * 16 + threadIdx.x / 16, l = threadIdx.x % 16;
+  float v = 0.f;
+  if (o < a.M * ncols) {
+    const int m = o / ncols, c = o % ncols;
+    for (int y = l; y < n_split; y += 16) v += a.part[((int64_t)y * 16 + m) * ncols + c];
   }
+#pragma unroll
+  for (int off = 8; off >= 1; off >>= 1) v += __shfl_xor(v, off, 16);
+  if (l != 0 || o >= a.M * ncols) return;
+  const int m = o / ncols, c = o % ncols;
+  const int t = c / a.rank_pad, j = c % a.rank_pad;
+  a.U[(int64_t)m * a.ldu + a.ucol[t] + j] = f2bf(v * a.scale[t]);
 }
 
 template <int NB>
@@ -126,7 +133,8 @@ void go(hipStream_t s, LdArgs a, float *ws, int64_t ws_floats) {
     a.spw = spw;
     a.part = ws;
     hipLaunchKernelGGL((lora_down_kernel<NB, UNROLL, 1>), dim3(1, n_split), dim3(256), 0, s, a);
-    hipLaunchKernelGGL(lora_down_sum_kernel, dim3(1), dim3(256), 0, s, a, n_split);
+    hipLaunchKernelGGL(lora_down_sum_kernel, dim3((a.M * a.n_targets * a.rank_pad + 15) / 16), dim3(256), 0, s, a,
+                       n_split);
     return;
   }
   a.spw = nsteps;
