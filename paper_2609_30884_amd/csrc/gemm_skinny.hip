@@ -18,6 +18,7 @@ namespace crf {
 namespace {
 
 constexpr int UNROLL = 8;  // k-steps of loads issued before their MFMAs
+constexpr int CUS = 256;   // compute units the launch shapes are sized for
 
 // Row `r` (tile space, as in gemm_bf16) of the weight matrix and its segment.
 CRF_DEV const bf16 *skinny_weight_row(const GemmParams &p, GemmEpi epi, int r, int block, int &seg, int &local) {
@@ -54,15 +55,18 @@ __global__ __launch_bounds__(64 * W) void gemm_skinny_kernel(const GemmParams p)
   f32x4 acc[NB];
 #pragma unroll
   for (int b = 0; b < NB; ++b) acc[b] = f32x4{0.f, 0.f, 0.f, 0.f};
-  // wave w takes k-steps w, w + W, ...; UNROLL of them are loaded before their
-  // MFMAs (the scheduling barrier keeps every load of a batch in flight at once)
+  // wave w takes the k-step pairs w, w + W, ... (a pair covers 128 bytes of
+  // each weight row: whole cache lines per wave); UNROLL steps are loaded
+  // before their MFMAs (the scheduling barrier keeps every load of a batch in
+  // flight at once)
   const int nsteps = p.K / 32;
-  for (int st = wave; st < nsteps; st += W * UNROLL) {
+  for (int sp = wave; 2 * sp < nsteps; sp += W * UNROLL / 2) {
     bf16x8 xb[UNROLL], wb[UNROLL][NB];
 #pragma unroll
     for (int u = 0; u < UNROLL; ++u) {
-      if (st + W * u < nsteps) {  // wave-uniform
-        const int k = (st + W * u) * 32;
+      const int st = 2 * (sp + W * (u / 2)) + u % 2;
+      if (st < nsteps) {  // wave-uniform
+        const int k = st * 32;
         xb[u] = as_bf16x8(ld16(xrow + k));
 #pragma unroll
         for (int b = 0; b < NB; ++b) wb[u][b] = as_bf16x8(ld16(wrow[b] + k));
@@ -71,7 +75,7 @@ __global__ __launch_bounds__(64 * W) void gemm_skinny_kernel(const GemmParams p)
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int u = 0; u < UNROLL; ++u)
-      if (st + W * u < nsteps)
+      if (2 * (sp + W * (u / 2)) + u % 2 < nsteps)
 #pragma unroll
         for (int b = 0; b < NB; ++b) acc[b] = mfma16(wb[u][b], xb[u], acc[b]);
   }
@@ -164,9 +168,11 @@ __global__ void qkv_post_bf16_kernel(const GemmParams p, int hd) {
 // whole grid to keep HBM busy when there are few 16-feature workgroups.
 template <int EPI, int NB>
 void launch_skinny(hipStream_t s, int n_wg, const GemmParams &p) {
-  if (n_wg >= 1024)
+  // about 16 resident waves per CU: one round of 16-wave workgroups up to one
+  // per CU, of 8-wave ones up to two per CU, else 4 waves (2 were no faster)
+  if (n_wg > 2 * CUS)
     hipLaunchKernelGGL((gemm_skinny_kernel<EPI, NB, 4>), dim3(n_wg), dim3(256), 0, s, p);
-  else if (n_wg >= 512)
+  else if (n_wg > CUS)
     hipLaunchKernelGGL((gemm_skinny_kernel<EPI, NB, 8>), dim3(n_wg), dim3(512), 0, s, p);
   else
     hipLaunchKernelGGL((gemm_skinny_kernel<EPI, NB, 16>), dim3(n_wg), dim3(1024), 0, s, p);
