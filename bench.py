@@ -30,6 +30,7 @@ if ROOT not in sys.path:
 METRIC = "recomputed token-layers/sec and ms per 16K-token window (7B-shape); MFMA util"
 SHAPE_NAME = {3584: "Qwen2.5-7B", 1536: "Qwen2.5-1.5B"}
 PEAK_BF16 = 2.5e15      # MI355X dense bf16 MFMA, FLOP/s
+PEAK_F32_VALU = 157.3e12  # MI355X fp32 vector FLOP/s (the fp32 path runs on plain FMAs)
 PEAK_HBM = 8.0e12       # bytes/s
 
 
@@ -218,6 +219,7 @@ def main():
     dom = max((k for k in kernels if k in kflops), key=lambda k: timing[k][0])
     dom_avg_s = timing[dom][0] / timing[dom][1] * 1e-3
     achieved = kflops[dom] / dom_avg_s
+    peak = PEAK_BF16 if dims.dtype == "bf16" else PEAK_F32_VALU
     traffic = None
     prof = os.path.join(ROOT, "profiles", f"traffic_{dom}_{wl.name}.json")
     if os.path.exists(prof):
@@ -249,11 +251,11 @@ def main():
             "n_tokens": win.n_tokens, "l0": win.l0, "h": win.h, "d_model": dims.d_model, "n_q_heads": dims.n_q_heads,
             "n_kv_heads": dims.n_kv_heads, "head_dim": dims.head_dim, "d_ffn": dims.d_ffn, "lora_rank": wl.lora_rank,
         },
-        "mfma_util": round(f_win / (elapsed / args.steps) / PEAK_BF16, 4),
+        "mfma_util": round(f_win / (elapsed / args.steps) / peak, 4),
         "window_tflops": round(f_win / (elapsed / args.steps) / 1e12, 1),
-        "roofline": {"bound": "mfma", "kernel": dom, "achieved": round(achieved / 1e12, 1),
-                     "peak": PEAK_BF16 / 1e12, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16, 4),
-                     "traffic": traffic},
+        "roofline": {"bound": "mfma" if dims.dtype == "bf16" else "alu", "kernel": dom,
+                     "achieved": round(achieved / 1e12, 1), "peak": round(peak / 1e12, 1), "unit": "TFLOP/s",
+                     "frac": round(achieved / peak, 4), "traffic": traffic},
         "kernels": kernels,
         "device": device,
     }
