@@ -123,8 +123,14 @@ int32_t crf_abi_version(void);
 /* Create a context for `dims` on the current HIP device.  Allocates the
  * workspace for windows of up to max_tokens prefix tokens and LoRA ranks up
  * to max_lora_rank, and the rotary angle table for positions
- * 0..max_tokens-1.  On success *out receives the context (destroy with
- * crf_context_destroy).  Errors: INVALID_ARG (null), UNSUPPORTED (see
+ * 0..max_tokens-1.  Besides the per-token buffers (fp32 residual stream,
+ * normalised input, queries, attention output, SwiGLU output, LoRA
+ * down-projections), a bf16 context holds fixed-size scratch for split
+ * work: one 256x256 fp32 tile per compute unit for the residual GEMMs' K-parts
+ * (64 MiB on 256 CUs), key-split attention partials for decoding steps
+ * (ceil(max_tokens/64) x n_q_heads x 16 x (head_dim+4) floats) and K-split
+ * LoRA partials.  All of it is freed by crf_context_destroy.  On success *out
+ * receives the context.  Errors: INVALID_ARG (null), UNSUPPORTED (see
  * crf_validate_dims), HIP (allocation failed). */
 crf_status crf_context_create(const crf_model_dims *dims, int32_t max_tokens, int32_t max_lora_rank,
                               crf_context **out);
