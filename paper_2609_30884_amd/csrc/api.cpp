@@ -297,9 +297,16 @@ crf_status run_layers_bf16(crf_context *ctx, const void *hb, const crf_layer_wei
     LoraDownTarget tg[3];
     // a few token rows (a decoding step, a very short window): weight-streaming kernels
     const bool skinny = M <= 16;
+    LoraSplit lsplit;  // set by the last LoRA down-projection
     auto gemm = [&](GemmEpi epi, GemmParams &p) {
       if (!skinny) return launch_gemm_bf16(s, epi, hd, p);
       p.proj = ctx->proj16;
+      if (p.U && lsplit.n_parts > 0) {  // U still as K-split partials: the projection sums them
+        p.upart = ctx->lora_part;
+        p.upart_n = lsplit.n_parts;
+        p.upart_cols = lsplit.cols;
+        p.uscale = scale;
+      }
       return launch_gemm_skinny_bf16(s, epi, hd, p);
     };
 
@@ -311,7 +318,7 @@ crf_status run_layers_bf16(crf_context *ctx, const void *hb, const crf_layer_wei
       // Nothing reads this layer's output: its cache entry depends only on its
       // input through the K and V projections, so only those run.
       const bool kv_any = lora_targets({CRF_K, CRF_V}, tg);
-      if (kv_any) LAUNCH(ctx, s, CRF_KK_LORA_DOWN, launch_lora_down_bf16(s, xn, D, M, D, tg, 2, rp, u, ldu, ctx->lora_part, ctx->lora_part_floats));
+      if (kv_any) LAUNCH(ctx, s, CRF_KK_LORA_DOWN, launch_lora_down_bf16(s, xn, D, M, D, tg, 2, rp, u, ldu, ctx->lora_part, ctx->lora_part_floats, &lsplit));
       GemmParams p = base_params(xn, D, 2 * dkv);
       p.w[1] = (const bf16 *)w.w[CRF_K];
       p.w[2] = (const bf16 *)w.w[CRF_V];
@@ -333,7 +340,7 @@ crf_status run_layers_bf16(crf_context *ctx, const void *hb, const crf_layer_wei
       break;
     }
     bool any = lora_targets({CRF_Q, CRF_K, CRF_V}, tg);
-    if (any) LAUNCH(ctx, s, CRF_KK_LORA_DOWN, launch_lora_down_bf16(s, xn, D, M, D, tg, 3, rp, u, ldu, ctx->lora_part, ctx->lora_part_floats));
+    if (any) LAUNCH(ctx, s, CRF_KK_LORA_DOWN, launch_lora_down_bf16(s, xn, D, M, D, tg, 3, rp, u, ldu, ctx->lora_part, ctx->lora_part_floats, &lsplit));
     {
       GemmParams p = base_params(xn, D, dq + 2 * dkv);
       p.w[0] = (const bf16 *)w.w[CRF_Q];
@@ -361,7 +368,7 @@ crf_status run_layers_bf16(crf_context *ctx, const void *hb, const crf_layer_wei
            launch_attn_bf16(s, q, layer_kv(ctx, kv, l), attn, M, pos0, d.n_q_heads, d.n_kv_heads, hd,
                             ctx->attn_part, ctx->attn_part_floats));
     any = lora_targets({CRF_O}, tg);
-    if (any) LAUNCH(ctx, s, CRF_KK_LORA_DOWN, launch_lora_down_bf16(s, attn, dq, M, dq, tg, 1, rp, u, ldu, ctx->lora_part, ctx->lora_part_floats));
+    if (any) LAUNCH(ctx, s, CRF_KK_LORA_DOWN, launch_lora_down_bf16(s, attn, dq, M, dq, tg, 1, rp, u, ldu, ctx->lora_part, ctx->lora_part_floats, &lsplit));
     {
       GemmParams p = base_params(attn, dq, D);
       p.w[0] = (const bf16 *)w.w[CRF_O];
@@ -378,7 +385,7 @@ crf_status run_layers_bf16(crf_context *ctx, const void *hb, const crf_layer_wei
     LAUNCH(ctx, s, CRF_KK_NORM,
            launch_rmsnorm(s, ctx->hres, true, w.mlp_norm, false, xn, false, nullptr, M, D, d.rms_eps));
     any = lora_targets({CRF_GATE, CRF_UP}, tg);
-    if (any) LAUNCH(ctx, s, CRF_KK_LORA_DOWN, launch_lora_down_bf16(s, xn, D, M, D, tg, 2, rp, u, ldu, ctx->lora_part, ctx->lora_part_floats));
+    if (any) LAUNCH(ctx, s, CRF_KK_LORA_DOWN, launch_lora_down_bf16(s, xn, D, M, D, tg, 2, rp, u, ldu, ctx->lora_part, ctx->lora_part_floats, &lsplit));
     {
       GemmParams p = base_params(xn, D, 2 * f);
       p.w[0] = (const bf16 *)w.w[CRF_GATE];
@@ -395,7 +402,7 @@ crf_status run_layers_bf16(crf_context *ctx, const void *hb, const crf_layer_wei
       LAUNCH(ctx, s, CRF_KK_GEMM_GATEUP, gemm(EPI_SWIGLU, p));
     }
     any = lora_targets({CRF_DOWN}, tg);
-    if (any) LAUNCH(ctx, s, CRF_KK_LORA_DOWN, launch_lora_down_bf16(s, act, f, M, f, tg, 1, rp, u, ldu, ctx->lora_part, ctx->lora_part_floats));
+    if (any) LAUNCH(ctx, s, CRF_KK_LORA_DOWN, launch_lora_down_bf16(s, act, f, M, f, tg, 1, rp, u, ldu, ctx->lora_part, ctx->lora_part_floats, &lsplit));
     {
       GemmParams p = base_params(act, f, D);
       p.w[0] = (const bf16 *)w.w[CRF_DOWN];

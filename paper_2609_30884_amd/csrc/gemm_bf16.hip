@@ -22,6 +22,7 @@
 // gate/up pair live in the same lane).  16-byte LDS chunks are XOR-swizzled by
 // (row/2) mod 8 so the fragment reads are bank-conflict free.
 #include <algorithm>
+#include <atomic>
 #include <type_traits>
 
 #include "kernels.hpp"
@@ -216,9 +217,12 @@ __global__ __launch_bounds__(64 * WAVES, 1) void gemm_bf16_kernel(const GemmPara
       for (int j = 0; j < NJ; ++j) {
         const int m = min(m0 + wm * WTM + 32 * j + l32, p.M - 1);
         const bf16 *urow = p.U + (int64_t)m * p.ldu + k;
-        // segments used by this wave: blocks 0,1 and 2,3 may differ (EPI_SWIGLU)
-        const bf16x8 u01 = as_bf16x8(ld16(urow + p.ucol[seg[0]]));
-        const bf16x8 u23 = as_bf16x8(ld16(urow + p.ucol[seg[2]]));
+        // segments used by this wave: blocks 0,1 and 2,3 may differ (EPI_SWIGLU);
+        // U columns past the rank stay unread (the factor side is zero there,
+        // and they may lie past the row or the buffer)
+        const u32x4 zero = {0u, 0u, 0u, 0u};
+        const bf16x8 u01 = as_bf16x8(k < p.rank ? ld16(urow + p.ucol[seg[0]]) : zero);
+        const bf16x8 u23 = as_bf16x8(k < p.rank ? ld16(urow + p.ucol[seg[2]]) : zero);
 #pragma unroll
         for (int i = 0; i < 4; ++i) acc[i][j] = mfma32(lbf[i], i < 2 ? u01 : u23, acc[i][j]);
       }
@@ -517,12 +521,17 @@ hipError_t go(hipStream_t s, const GemmParams &p0) {
   }
   const int grid = p.split_first + (tiles - p.split_first) * p.split_s;
   const size_t lds = (size_t)STAGES * (BM + BN) * BK * sizeof(bf16);
-  static bool attr_set = false;
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void *)gemm_bf16_kernel<EPI, HD, WAVES>,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  // the dynamic-LDS limit is raised once per device (bit d of attr_set)
+  static std::atomic<uint64_t> attr_set{0};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  const uint64_t bit = dev < 64 ? (uint64_t)1 << dev : 0;
+  if (!bit || !(attr_set.load() & bit)) {
+    e = hipFuncSetAttribute((const void *)gemm_bf16_kernel<EPI, HD, WAVES>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)lds);
     if (e != hipSuccess) return e;
-    attr_set = true;
+    attr_set.fetch_or(bit);
   }
   hipLaunchKernelGGL((gemm_bf16_kernel<EPI, HD, WAVES>), dim3(grid), dim3(64 * WAVES), lds, s, p);
   if (p.split_s > 1) {

@@ -18,7 +18,6 @@ namespace crf {
 namespace {
 
 constexpr int UNROLL = 8;  // k-steps of loads issued before their MFMAs
-constexpr int CUS = 256;   // compute units the launch shapes are sized for
 
 // Row `r` (tile space, as in gemm_bf16) of the weight matrix and its segment.
 CRF_DEV const bf16 *skinny_weight_row(const GemmParams &p, GemmEpi epi, int r, int block, int &seg, int &local) {
@@ -99,7 +98,21 @@ __global__ __launch_bounds__(64 * W) void gemm_skinny_kernel(const GemmParams p)
         const int j = kk + kq;
         u32x4 av = {0u, 0u, 0u, 0u}, uv = {0u, 0u, 0u, 0u};
         if (j < p.rank) av = ld16(lb + (int64_t)local[b] * p.rank + j);
-        if (j < p.kpad) uv = ld16(p.U + (int64_t)tok * p.ldu + p.ucol[seg[b]] + j);
+        if (j < p.rank && p.upart_n > 0) {  // sum the K-split partials in part order
+          const float *pp = p.upart + (int64_t)tok * p.upart_cols + p.ucol[seg[b]] + j;
+          f32x4 lo = {0.f, 0.f, 0.f, 0.f}, hi = {0.f, 0.f, 0.f, 0.f};
+          for (int y = 0; y < p.upart_n; ++y) {
+            lo += *reinterpret_cast<const f32x4 *>(pp + (int64_t)y * 16 * p.upart_cols);
+            hi += *reinterpret_cast<const f32x4 *>(pp + (int64_t)y * 16 * p.upart_cols + 4);
+          }
+          lo *= p.uscale;
+          hi *= p.uscale;
+          const bf16x8 u8 = {f2bf(lo[0]), f2bf(lo[1]), f2bf(lo[2]), f2bf(lo[3]),
+                             f2bf(hi[0]), f2bf(hi[1]), f2bf(hi[2]), f2bf(hi[3])};
+          uv = as_u32x4(u8);
+        } else if (j < p.rank) {  // (past the rank: unread)
+          uv = ld16(p.U + (int64_t)tok * p.ldu + p.ucol[seg[b]] + j);
+        }
         acc[b] = mfma16(as_bf16x8(av), as_bf16x8(uv), acc[b]);
       }
     }
@@ -168,6 +181,7 @@ __global__ void qkv_post_bf16_kernel(const GemmParams p, int hd) {
 // whole grid to keep HBM busy when there are few 16-feature workgroups.
 template <int EPI, int NB>
 void launch_skinny(hipStream_t s, int n_wg, const GemmParams &p) {
+  const int CUS = p.n_cu > 0 ? p.n_cu : 256;  // compute units of the device
   // about 16 resident waves per CU: one round of 16-wave workgroups up to one
   // per CU, of 8-wave ones up to two per CU, else 4 waves (2 were no faster)
   if (n_wg > 2 * CUS)

@@ -37,9 +37,17 @@ struct LoraDownTarget {
 // U[m, ucol_t + j] = bf16(scale_t * sum_k X[m,k] A_t[j,k]) for j < rank_pad(t)
 // (zero for rank <= j < rank_pad).
 // ws (nullable, ws_floats floats): workspace for splitting K over workgroups
-// when M <= 16.
+// when M <= 16.  With `split` non-null, a split into at most four parts is
+// left as unscaled fp32 partials in ws ([part][16][n_targets * rank_pad]) for
+// the consuming projection to sum (split->n_parts > 0; U is not written);
+// otherwise split->n_parts = 0 and U holds the result.
+struct LoraSplit {
+  int n_parts = 0;
+  int cols = 0;
+};
 hipError_t launch_lora_down_bf16(hipStream_t s, const bf16 *X, int64_t ldx, int M, int K, const LoraDownTarget *t,
-                                 int n_targets, int rank_pad, bf16 *U, int ldu, float *ws, int64_t ws_floats);
+                                 int n_targets, int rank_pad, bf16 *U, int ldu, float *ws, int64_t ws_floats,
+                                 LoraSplit *split = nullptr);
 
 enum GemmEpi { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2 };
 
@@ -73,6 +81,11 @@ struct GemmParams {
   int d_ffn;
   // EPI_QKV with few token rows: fp32 projections [M, N] before the rotary/paged stores
   float *proj;
+  // few token rows: U given as unscaled K-split partials ([part][16][upart_cols]
+  // fp32, upart_n parts) to be summed, scaled by uscale and rounded to bf16
+  const float *upart;
+  int upart_n, upart_cols;
+  float uscale;
   // EPI_RESID: when the tiles leave the last wave of the grid at most half
   // full (n_cu compute units), the last tiles are split into K-parts that
   // write fp32 partials to split_part (split_cap floats) and a second kernel

@@ -123,7 +123,7 @@ __global__ __launch_bounds__(256) void lora_down_sum_kernel(LdArgs a, int n_spli
 }
 
 template <int NB>
-void go(hipStream_t s, LdArgs a, float *ws, int64_t ws_floats) {
+void go(hipStream_t s, LdArgs a, float *ws, int64_t ws_floats, LoraSplit *split) {
   constexpr int UNROLL = NB <= 4 ? 8 : 2;
   const int nsteps = a.K / 32;
   // a few token rows: split K over workgroups (one batch of loads per wave)
@@ -133,6 +133,11 @@ void go(hipStream_t s, LdArgs a, float *ws, int64_t ws_floats) {
     a.spw = spw;
     a.part = ws;
     hipLaunchKernelGGL((lora_down_kernel<NB, UNROLL, 1>), dim3(1, n_split), dim3(256), 0, s, a);
+    if (split && n_split <= 4) {  // the consumer sums the partials
+      split->n_parts = n_split;
+      split->cols = a.n_targets * a.rank_pad;
+      return;
+    }
     hipLaunchKernelGGL(lora_down_sum_kernel, dim3((a.M * a.n_targets * a.rank_pad + 15) / 16), dim3(256), 0, s, a,
                        n_split);
     return;
@@ -151,7 +156,9 @@ void go(hipStream_t s, LdArgs a, float *ws, int64_t ws_floats) {
 }  // namespace
 
 hipError_t launch_lora_down_bf16(hipStream_t s, const bf16 *X, int64_t ldx, int M, int K, const LoraDownTarget *t,
-                                 int n_targets, int rank_pad, bf16 *U, int ldu, float *ws, int64_t ws_floats) {
+                                 int n_targets, int rank_pad, bf16 *U, int ldu, float *ws, int64_t ws_floats,
+                                 LoraSplit *split) {
+  if (split) *split = LoraSplit{};
   if (M <= 0 || n_targets <= 0) return hipSuccess;
   if (n_targets > MAXT || n_targets * rank_pad > MAXB * 16 || rank_pad % 16 || K % 32) return hipErrorInvalidValue;
   LdArgs a{};
@@ -170,14 +177,14 @@ hipError_t launch_lora_down_bf16(hipStream_t s, const bf16 *X, int64_t ldx, int 
   a.U = U;
   a.ldu = ldu;
   switch (n_targets * rank_pad / 16) {
-    case 1: go<1>(s, a, ws, ws_floats); break;
-    case 2: go<2>(s, a, ws, ws_floats); break;
-    case 3: go<3>(s, a, ws, ws_floats); break;
-    case 4: go<4>(s, a, ws, ws_floats); break;
-    case 6: go<6>(s, a, ws, ws_floats); break;
-    case 8: go<8>(s, a, ws, ws_floats); break;
-    case 9: go<9>(s, a, ws, ws_floats); break;
-    case 12: go<12>(s, a, ws, ws_floats); break;
+    case 1: go<1>(s, a, ws, ws_floats, split); break;
+    case 2: go<2>(s, a, ws, ws_floats, split); break;
+    case 3: go<3>(s, a, ws, ws_floats, split); break;
+    case 4: go<4>(s, a, ws, ws_floats, split); break;
+    case 6: go<6>(s, a, ws, ws_floats, split); break;
+    case 8: go<8>(s, a, ws, ws_floats, split); break;
+    case 9: go<9>(s, a, ws, ws_floats, split); break;
+    case 12: go<12>(s, a, ws, ws_floats, split); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
