@@ -27,6 +27,10 @@ struct Timer {
 
 }  // namespace
 
+// runs of consecutive gate/up tiles on one token tile per workgroup whose fused
+// down-projection adapter sums the context holds room for
+constexpr int DN_RUNS = 4;
+
 struct crf_context {
   crf_model_dims dims;
   int32_t max_tokens = 0, max_rank = 0, rank_pad = 0;
@@ -50,6 +54,8 @@ struct crf_context {
   int64_t lora_part_floats = 0;
   float *gemm_part = nullptr;  // bf16 path: K-part partials of the last residual GEMM tiles
   int64_t gemm_part_floats = 0;
+  float *dn_part = nullptr;    // bf16 path: down-projection adapter sums fused into gate/up
+  int *dn_head = nullptr;      //   and the table of their first tiles
   int n_cu = 0;
   // drift staging
   void *drift_host = nullptr;
@@ -386,8 +392,12 @@ crf_status run_layers_bf16(crf_context *ctx, const void *hb, const crf_layer_wei
            launch_rmsnorm(s, ctx->hres, true, w.mlp_norm, false, xn, false, nullptr, M, D, d.rms_eps));
     any = lora_targets({CRF_GATE, CRF_UP}, tg);
     if (any) LAUNCH(ctx, s, CRF_KK_LORA_DOWN, launch_lora_down_bf16(s, xn, D, M, D, tg, 2, rp, u, ldu, ctx->lora_part, ctx->lora_part_floats, &lsplit));
+    // the down projection's adapter down-projection rides on the gate/up
+    // epilogue when its rank fits (dn_done), else it is a pass of its own
+    bool dn_done = false;
+    GemmParams pgu = base_params(xn, D, 2 * f);
     {
-      GemmParams p = base_params(xn, D, 2 * f);
+      GemmParams &p = pgu;
       p.w[0] = (const bf16 *)w.w[CRF_GATE];
       p.w[1] = (const bf16 *)w.w[CRF_UP];
       if (any) {
@@ -399,10 +409,20 @@ crf_status run_layers_bf16(crf_context *ctx, const void *hb, const crf_layer_wei
       }
       p.act = act;
       p.d_ffn = f;
-      LAUNCH(ctx, s, CRF_KK_GEMM_GATEUP, gemm(EPI_SWIGLU, p));
+      if (!skinny && has_lora(lora, l, CRF_DOWN) && rank <= 16 && ctx->dn_part) {
+        p.dn_a = (const bf16 *)lora[l].A[CRF_DOWN];
+        p.dn_rank = rank;
+        p.dn_part = ctx->dn_part;
+        p.dn_head = ctx->dn_head;
+        p.dn_runs = DN_RUNS;
+      }
+      LAUNCH(ctx, s, CRF_KK_GEMM_GATEUP, skinny ? gemm(EPI_SWIGLU, p) : launch_gemm_bf16(s, EPI_SWIGLU, hd, p, &dn_done));
     }
     any = lora_targets({CRF_DOWN}, tg);
-    if (any) LAUNCH(ctx, s, CRF_KK_LORA_DOWN, launch_lora_down_bf16(s, act, f, M, f, tg, 1, rp, u, ldu, ctx->lora_part, ctx->lora_part_floats, &lsplit));
+    if (any && dn_done)
+      LAUNCH(ctx, s, CRF_KK_LORA_DOWN, launch_gemm_dn_sum(s, pgu, u, ldu, 0, scale));
+    else if (any)
+      LAUNCH(ctx, s, CRF_KK_LORA_DOWN, launch_lora_down_bf16(s, act, f, M, f, tg, 1, rp, u, ldu, ctx->lora_part, ctx->lora_part_floats, &lsplit));
     {
       GemmParams p = base_params(act, f, D);
       p.w[0] = (const bf16 *)w.w[CRF_DOWN];
@@ -518,7 +538,8 @@ crf_status crf_validate_window(const crf_model_dims *dims, int32_t l0, int32_t h
 void crf_context_destroy(crf_context *ctx) {
   if (!ctx) return;
   void *bufs[] = {ctx->hres, ctx->xn, ctx->q, ctx->attn, ctx->act, ctx->u, ctx->proj, ctx->gu, ctx->rope_cs,
-                  ctx->d_err, ctx->drift_dev, ctx->proj16, ctx->attn_part, ctx->lora_part, ctx->gemm_part};
+                  ctx->d_err, ctx->drift_dev, ctx->proj16, ctx->attn_part, ctx->lora_part, ctx->gemm_part,
+                  ctx->dn_part, ctx->dn_head};
   for (void *b : bufs)
     if (b) (void)hipFree(b);
   if (ctx->drift_host) (void)hipHostFree(ctx->drift_host);
@@ -572,6 +593,14 @@ crf_status crf_context_create(const crf_model_dims *dims, int32_t max_tokens, in
     if (ctx->gemm_part_floats > 0 &&
         (st = dmalloc(ctx, &ctx->gemm_part, (size_t)ctx->gemm_part_floats * 4)) != CRF_OK)
       return cleanup(st);
+    // fused down-projection adapter sums: DN_RUNS runs of [2][256][16] per
+    // compute unit, and one table entry per gate/up tile
+    if (ctx->n_cu > 0 && max_lora_rank > 0) {
+      if ((st = dmalloc(ctx, &ctx->dn_part, (size_t)ctx->n_cu * DN_RUNS * 2 * 256 * 16 * 4)) != CRF_OK)
+        return cleanup(st);
+      if ((st = dmalloc(ctx, &ctx->dn_head, ((T + 255) / 256) * ((2 * f + 255) / 256) * sizeof(int))) != CRF_OK)
+        return cleanup(st);
+    }
   } else {
     if ((st = dmalloc(ctx, &ctx->u, T * (size_t)(max_lora_rank > 0 ? max_lora_rank : 1) * 4)) != CRF_OK)
       return cleanup(st);

@@ -5,22 +5,25 @@
 //   EPI_QKV    bias + rotary rotation of Q and K, Q to a [M, dq] buffer, K and V
 //              straight into the layer's pages of the paged cache;
 //   EPI_RESID  fp32 residual update (attention output / down projection);
-//   EPI_SWIGLU silu(gate) * up with gate and up rows interleaved per 64 features.
+//   EPI_SWIGLU silu(gate) * up with gate and up rows interleaved per 64 features,
+//              optionally also the down projection's adapter down-projection
+//              act . A_down^T, summed over the features a workgroup produces.
 //
-// Tiling for CDNA4: a 256x256 output tile per workgroup, either 4 waves of
-// 128x128 (one wave per SIMD) or 8 waves of 128x64 (two waves per SIMD, so one
-// wave issues MFMAs while the other waits on LDS or memory); every wave owns
-// 128 output features.  v_mfma_f32_32x32x16_bf16; K staged through LDS in
-// 64-wide slices, double-buffered (2 x 64 KB).  Slices move global -> LDS by
-// DMA (buffer_load ... lds): no staging registers and no LDS stores in the
-// waves' instruction stream; slice kt+2's DMA is issued right after the single
-// per-slice barrier and overlaps slice kt+1's MFMAs, and fragment reads run one
-// MFMA group ahead.  Rows past M (or past N) get an out-of-range offset and
-// arrive as zeros.  The weight operand takes the MFMA "A"
-// role so each lane ends up holding 4 consecutive output features of one
+// Tiling for CDNA4: a 256x256 output tile per work item, 8 waves of 128x64 (two
+// waves per SIMD, so one wave issues MFMAs while the other waits on LDS or
+// memory); every wave owns 128 output features.  v_mfma_f32_32x32x16_bf16; K
+// staged through LDS in 64-wide slices, double-buffered (2 x 64 KB).  Slices
+// move global -> LDS by DMA (buffer_load ... lds): no staging registers and no
+// LDS stores in the waves' instruction stream.  Rows past M (or past N) get an
+// out-of-range offset and arrive as zeros.  The weight operand takes the MFMA
+// "A" role so each lane ends up holding 4 consecutive output features of one
 // token, which makes every epilogue lane-local (a rotary pair (f, f+hd/2) and a
 // gate/up pair live in the same lane).  16-byte LDS chunks are XOR-swizzled by
 // (row/2) mod 8 so the fragment reads are bank-conflict free.
+//
+// Persistent: one workgroup per CU walks its share of the work items, and the
+// DMA cursor runs ahead across item boundaries, so the next item's first slices
+// load during this item's epilogue.
 #include <algorithm>
 #include <atomic>
 #include <type_traits>
@@ -36,9 +39,6 @@ namespace {
 #ifndef CRF_GEMM_STAGES
 #define CRF_GEMM_STAGES 2
 #endif
-#ifndef CRF_GEMM_WAVES
-#define CRF_GEMM_WAVES 8
-#endif
 
 constexpr int BM = 256, BN = 256;
 constexpr int BK = CRF_GEMM_BK;          // k-width of one LDS slice
@@ -46,8 +46,13 @@ constexpr int STAGES = CRF_GEMM_STAGES;  // slices resident in LDS (STAGES * 32 
 constexpr int GROUP_M = 8;
 constexpr int LPR = BK / 8;              // 16-byte chunks (lanes) per row of a slice
 constexpr int RPB = 64 / LPR;            // rows per 1 KB DMA block
+constexpr int WAVES = 8;
+constexpr int STAGE_BYTES = STAGES * (BM + BN) * BK * 2;
+// fused down-projection adapter sums: [2 feature halves][256 tokens][16 ranks] fp32
+constexpr int DN_RANK = 16;
+constexpr int DN_BYTES = 2 * BM * DN_RANK * 4;
 static_assert(BK == 32 || BK == 64, "slice width");
-static_assert(STAGES >= 2 && STAGES * (BM + BN) * BK * 2 <= 160 * 1024, "LDS budget");
+static_assert(STAGES >= 2 && STAGE_BYTES <= 160 * 1024, "LDS budget");
 
 // Chunk c of slice row r sits at position c ^ s(r), s(r) = (r / 2) % 8 for
 // 128-byte rows and (r / 4) % 4 for 64-byte rows: the 16 rows one quarter of a
@@ -62,20 +67,7 @@ CRF_DEV void wait_vm() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
-template <int EPI>
-CRF_DEV const bf16 *weight_row(const GemmParams &p, int r) {
-  if (EPI == EPI_RESID) return p.w[0] + (int64_t)r * p.K;
-  if (EPI == EPI_QKV) {
-    if (r < p.seg1) return p.w[0] + (int64_t)r * p.K;
-    if (r < p.seg2) return p.w[1] + (int64_t)(r - p.seg1) * p.K;
-    return p.w[2] + (int64_t)(r - p.seg2) * p.K;
-  }
-  // EPI_SWIGLU: 128 tile rows per 64 output features: [gate f..f+64, up f..f+64]
-  const int f = (r >> 7) * 64 + (r & 63);
-  return p.w[(r >> 6) & 1] + (int64_t)f * p.K;
-}
-
-// Segment and in-segment row of tile-space row r (used for LoRA factors and biases).
+// Segment and in-segment row of tile-space row r (used for weights, LoRA factors and biases).
 template <int EPI>
 CRF_DEV int segment_of(const GemmParams &p, int r, int &local) {
   if (EPI == EPI_RESID) { local = r; return 0; }
@@ -85,26 +77,83 @@ CRF_DEV int segment_of(const GemmParams &p, int r, int &local) {
     local = r - p.seg2;
     return 2;
   }
+  // EPI_SWIGLU: 128 tile rows per 64 output features: [gate f..f+64, up f..f+64]
   local = (r >> 7) * 64 + (r & 63);
   return (r >> 6) & 1;
 }
 
+// ---- work items.  Shared by the kernel and the host (fused-sum slot count).
+//
+// A work item is a whole 256x256 tile (part -1) or K-part `part` of one of the
+// split tiles, over K slices [kb, ke).  Whole tiles come first in item order
+// and K-parts after them; each range is remapped on its own so that every XCD
+// gets an equal, contiguous share of both (workgroup b runs on XCD b % 8).
+struct WorkItem {
+  int w, t, part, kb, ke, tm, tn;
+};
+
+__host__ __device__ inline int xcd_map(int i, int n) {
+  return n % 8 ? i : (i % 8) * (n / 8) + i / 8;
+}
+
 // Tile t of the grouped order (GROUP_M token tiles share a weight panel).
-CRF_DEV void tile_coords(int t, int tiles_m, int tiles_n, int &tm, int &tn) {
+__host__ __device__ inline void tile_coords(int t, int tiles_m, int tiles_n, int &tm, int &tn) {
   const int group = GROUP_M * tiles_n;
   const int first_m = (t / group) * GROUP_M;
-  const int gm = min(tiles_m - first_m, GROUP_M);
+  const int gm = tiles_m - first_m < GROUP_M ? tiles_m - first_m : GROUP_M;
   tm = first_m + (t % group) % gm;
   tn = (t % group) / gm;
 }
 
-// WAVES = 4: 2 (features) x 2 (tokens) waves of 128 x 128.
-// WAVES = 8: 2 (features) x 4 (tokens) waves of 128 x 64.
-template <int EPI, int HD, int WAVES>
-__global__ __launch_bounds__(64 * WAVES, 1) void gemm_bf16_kernel(const GemmParams p) {
-  constexpr int NT = 64 * WAVES;
-  constexpr int WM_COUNT = WAVES / 2;      // token groups
-  constexpr int WTM = BM / WM_COUNT;       // tokens per wave: 128 or 64
+struct Sched {
+  int tiles_m, tiles_n, nk, n_items, split_first, split_s, grid;
+  bool stagger;  // odd workgroups take their last item (a K-part) first
+};
+
+__host__ __device__ inline int n_mine(const Sched &s, int b) {
+  return b < s.n_items ? (s.n_items - 1 - b) / s.grid + 1 : 0;
+}
+
+// i-th work item of workgroup b
+__host__ __device__ inline WorkItem work_item(const Sched &s, int b, int i) {
+  const int mine = n_mine(s, b);
+  int k = i;
+  if (s.stagger && (b & 1) && mine > 1) k = i == 0 ? mine - 1 : i - 1;
+  const int raw = b + k * s.grid;
+  WorkItem it;
+  it.part = -1;
+  it.kb = 0;
+  it.ke = s.nk;
+  if (s.split_s > 1 && raw >= s.split_first) {
+    const int n_parts = s.n_items - s.split_first;
+    it.w = s.split_first + xcd_map(raw - s.split_first, n_parts);
+    it.t = s.split_first + (it.w - s.split_first) / s.split_s;
+    it.part = (it.w - s.split_first) % s.split_s;
+    it.kb = it.part * s.nk / s.split_s;
+    it.ke = (it.part + 1) * s.nk / s.split_s;
+  } else {
+    it.w = xcd_map(raw, s.split_s > 1 ? s.split_first : s.n_items);
+    it.t = it.w;
+  }
+  tile_coords(it.t, s.tiles_m, s.tiles_n, it.tm, it.tn);
+  return it;
+}
+
+// Runs (maximal sequences of consecutive items on one token tile) of workgroup b.
+inline int n_runs(const Sched &s, int b) {
+  int runs = 0, tm = -1;
+  for (int i = 0; i < n_mine(s, b); ++i) {
+    const WorkItem it = work_item(s, b, i);
+    if (it.tm != tm) ++runs;
+    tm = it.tm;
+  }
+  return runs;
+}
+
+template <int EPI, int HD>
+__global__ __launch_bounds__(64 * WAVES, 1) void gemm_bf16_kernel(const GemmParams p, const Sched sc) {
+  constexpr int WM_COUNT = 4;              // token groups
+  constexpr int WTM = BM / WM_COUNT;       // tokens per wave
   constexpr int NJ = WTM / 32;             // 32-token blocks per wave
   constexpr int BLK = (BM / RPB) / WAVES;  // 1 KB DMA blocks per operand per wave per slice
   constexpr int DMA_PER_SLICE = 2 * BLK;
@@ -112,80 +161,93 @@ __global__ __launch_bounds__(64 * WAVES, 1) void gemm_bf16_kernel(const GemmPara
   bf16 *const lds_x = smem;                       // [STAGES][BM*BK]
   bf16 *const lds_w = smem + STAGES * BM * BK;    // [STAGES][BN*BK]
 
-  const int tiles_m = (p.M + BM - 1) / BM;
-  const int tiles_n = (p.N + BN - 1) / BN;
-  const int nk = p.K / BK;
-  // work item: a whole tile, or K-part `part` of one of the last tiles.  The
-  // whole tiles come first in dispatch order and the K-parts after them, each
-  // range remapped on its own so that every XCD gets an equal, contiguous
-  // share of both.
-  int w, t, part = -1, kb = 0, ke = nk;
-  if (EPI == EPI_RESID && p.split_s > 1 && (int)blockIdx.x >= p.split_first) {
-    const int n_parts = (int)gridDim.x - p.split_first;
-    w = p.split_first + xcd_remap((int)blockIdx.x - p.split_first, n_parts);
-    t = p.split_first + (w - p.split_first) / p.split_s;
-    part = (w - p.split_first) % p.split_s;
-    kb = part * nk / p.split_s;
-    ke = (part + 1) * nk / p.split_s;
-  } else {
-    w = xcd_remap(blockIdx.x, EPI == EPI_RESID && p.split_s > 1 ? p.split_first : gridDim.x);
-    t = w;
-  }
-  int tm, tn;
-  tile_coords(t, tiles_m, tiles_n, tm, tn);
-  const int m0 = tm * BM, n0 = tn * BN;
-
+  const int b = blockIdx.x;
   const int tid = threadIdx.x, lane = tid % 64;
   const int wave = __builtin_amdgcn_readfirstlane(tid / 64);  // uniform: keeps DMA targets scalar
   const int wn = wave / WM_COUNT, wm = wave % WM_COUNT;
   const int g = lane / 32, l32 = lane % 32;
+  const int mine = n_mine(sc, b);
 
-  // ---- global -> LDS DMA.  A slice of one operand is 256 rows x BK k = BK/2
-  // blocks of 1 KB; wave w moves blocks WAVES*j + w.  Inside a block, lane L
-  // writes LDS bytes [16 L, 16 L + 16): row RPB*block + L/LPR, swizzled
-  // position L%LPR, which holds the logical k-chunk at that position of swz.
+  // ---- producer: the global -> LDS DMA cursor runs STAGES slices ahead of
+  // the MFMAs and carries on into the workgroup's next item.  A slice of one
+  // operand is 256 rows x BK k = BK/2 blocks of 1 KB; wave w moves blocks
+  // WAVES*j + w.  Inside a block, lane L writes LDS bytes [16 L, 16 L + 16):
+  // row RPB*block + L/LPR, swizzled position L%LPR, which holds the logical
+  // k-chunk at that position of swz.
   const __amdgpu_buffer_rsrc_t xres = make_rsrc(p.X, (uint32_t)((int64_t)p.M * p.ldx * 2));
   uint32_t xoff[BLK], woff[BLK];
   __amdgpu_buffer_rsrc_t wres[BLK];
-#pragma unroll
-  for (int j = 0; j < BLK; ++j) {
-    const int blk = WAVES * j + wave;
-    const int row = blk * RPB + lane / LPR;
-    const int c = BK == 64 ? (lane % 8) ^ ((row >> 1) & 7) : (lane % 4) ^ ((row >> 2) & 3);
-    const int xr = m0 + row;
-    xoff[j] = xr < p.M ? (uint32_t)(((int64_t)xr * p.ldx + c * 8) * 2) : CRF_OOB;
-    // weight rows: the RPB rows of a block sit in one 64-row group, inside one segment
-    const int wr = n0 + row;
-    int lr0, local;
-    const int sg = segment_of<EPI>(p, min(n0 + blk * RPB, p.N - 1), lr0);
-    const int seg_rows = EPI == EPI_QKV ? (sg == 0 ? p.seg1 : sg == 1 ? p.seg2 - p.seg1 : p.N - p.seg2)
-                                        : (EPI == EPI_SWIGLU ? p.N / 2 : p.N);
-    segment_of<EPI>(p, min(wr, p.N - 1), local);
-    wres[j] = make_rsrc(p.w[sg], (uint32_t)((int64_t)seg_rows * p.K * 2));
-    woff[j] = wr < p.N ? (uint32_t)(((int64_t)local * p.K + c * 8) * 2) : CRF_OOB;
-  }
-  auto dma = [&](int k0, int stage) {
-    lds_char *dx = (lds_char *)(lds_x + stage * BM * BK);
-    lds_char *dw = (lds_char *)(lds_w + stage * BN * BK);
+  int pi = 0, pk = 0, pke = 0;  // item index and slice of the cursor
+  auto producer_setup = [&](int i) {
+    const WorkItem it = work_item(sc, b, i);
+    const int m0 = it.tm * BM, n0 = it.tn * BN;
+    pk = it.kb;
+    pke = it.ke;
 #pragma unroll
     for (int j = 0; j < BLK; ++j) {
       const int blk = WAVES * j + wave;
-      dma16(xres, dx + blk * 1024, xoff[j], (uint32_t)k0 * 2);
-      dma16(wres[j], dw + blk * 1024, woff[j], (uint32_t)k0 * 2);
+      const int row = blk * RPB + lane / LPR;
+      const int c = BK == 64 ? (lane % 8) ^ ((row >> 1) & 7) : (lane % 4) ^ ((row >> 2) & 3);
+      const int xr = m0 + row;
+      xoff[j] = xr < p.M ? (uint32_t)(((int64_t)xr * p.ldx + c * 8) * 2) : CRF_OOB;
+      // weight rows: the RPB rows of a block sit in one 64-row group, inside one segment
+      const int wr = n0 + row;
+      int lr0, local;
+      const int sg = segment_of<EPI>(p, min(n0 + blk * RPB, p.N - 1), lr0);
+      const int seg_rows = EPI == EPI_QKV ? (sg == 0 ? p.seg1 : sg == 1 ? p.seg2 - p.seg1 : p.N - p.seg2)
+                                          : (EPI == EPI_SWIGLU ? p.N / 2 : p.N);
+      segment_of<EPI>(p, min(wr, p.N - 1), local);
+      wres[j] = make_rsrc(p.w[sg], (uint32_t)((int64_t)seg_rows * p.K * 2));
+      woff[j] = wr < p.N ? (uint32_t)(((int64_t)local * p.K + c * 8) * 2) : CRF_OOB;
     }
   };
-  // blocks [J0, J1) of both operands
-  auto dma_part = [&](int k0, int stage, auto j0, auto j1) {
-    constexpr int J0 = decltype(j0)::value, J1 = decltype(j1)::value;
+  // one slice into `stage` (past the last item the cursor stays on the last
+  // slice: those copies are never consumed)
+  auto produce = [&](int stage) {
     lds_char *dx = (lds_char *)(lds_x + stage * BM * BK);
     lds_char *dw = (lds_char *)(lds_w + stage * BN * BK);
+    const uint32_t k0 = (uint32_t)pk * BK * 2;
 #pragma unroll
-    for (int j = J0; j < J1; ++j) {
+    for (int j = 0; j < BLK; ++j) {
       const int blk = WAVES * j + wave;
-      dma16(xres, dx + blk * 1024, xoff[j], (uint32_t)k0 * 2);
-      dma16(wres[j], dw + blk * 1024, woff[j], (uint32_t)k0 * 2);
+      dma16(xres, dx + blk * 1024, xoff[j], k0);
+      dma16(wres[j], dw + blk * 1024, woff[j], k0);
     }
   };
+  auto advance = [&]() {
+    if (++pk == pke) {
+      if (pi + 1 < mine) {
+        producer_setup(++pi);
+      } else {
+        pk = pke - 1;
+      }
+    }
+  };
+
+  // ---- fused down-projection adapter sums (EPI_SWIGLU with p.dn_a): wave
+  // (wn, wm) owns tokens [64 wm, 64 wm + 64) of half wn of the LDS sums, so the
+  // read-add-write below needs no synchronisation.
+  float *const dn_lds = (float *)((char *)smem + STAGE_BYTES);
+  const bool dn_on = EPI == EPI_SWIGLU && p.dn_a;
+  auto dn_zero = [&]() {
+    float *d = dn_lds + ((wn * BM + wm * WTM + lane) * DN_RANK);
+#pragma unroll
+    for (int r = 0; r < DN_RANK; r += 4) *reinterpret_cast<f32x4 *>(d + r) = f32x4{0.f, 0.f, 0.f, 0.f};
+  };
+  // the sums of a run on token tile tm go to slot `slot`: [slot][wn][256][16]
+  auto dn_flush = [&](int tm, int slot) {
+    const int ml = wm * WTM + lane, m = tm * BM + ml;
+    float *d = dn_lds + ((wn * BM + ml) * DN_RANK);
+    float *o = p.dn_part + (((int64_t)slot * 2 + wn) * BM + ml) * DN_RANK;
+    float z;  // materialised here: a hoisted zero vector would be spilled
+    asm volatile("v_mov_b32 %0, 0" : "=v"(z));
+#pragma unroll
+    for (int r = 0; r < DN_RANK; r += 4) {
+      if (m < p.M) *reinterpret_cast<f32x4 *>(o + r) = *reinterpret_cast<f32x4 *>(d + r);
+      *reinterpret_cast<f32x4 *>(d + r) = f32x4{z, z, z, z};
+    }
+  };
+  if (dn_on) dn_zero();
 
   f32x16 acc[4][NJ];
 #pragma unroll
@@ -195,43 +257,8 @@ __global__ __launch_bounds__(64 * WAVES, 1) void gemm_bf16_kernel(const GemmPara
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-  // ---- low-rank delta: acc += U[token, ucol_s + k] * lb_s[feature, k] (K-part 0 only)
-  if (p.U && part <= 0) {
-    int seg[4], frow[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int r = min(n0 + wn * 128 + 32 * i + l32, p.N - 1);
-      seg[i] = segment_of<EPI>(p, r, frow[i]);
-    }
-    for (int kk = 0; kk < p.kpad; kk += 16) {
-      const int k = kk + 8 * g;
-      bf16x8 lbf[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        u32x4 v = {0u, 0u, 0u, 0u};
-        const bf16 *lb = p.lb[seg[i]];
-        if (lb && k < p.rank) v = ld16(lb + (int64_t)frow[i] * p.rank + k);
-        lbf[i] = as_bf16x8(v);
-      }
-#pragma unroll
-      for (int j = 0; j < NJ; ++j) {
-        const int m = min(m0 + wm * WTM + 32 * j + l32, p.M - 1);
-        const bf16 *urow = p.U + (int64_t)m * p.ldu + k;
-        // segments used by this wave: blocks 0,1 and 2,3 may differ (EPI_SWIGLU);
-        // U columns past the rank stay unread (the factor side is zero there,
-        // and they may lie past the row or the buffer)
-        const u32x4 zero = {0u, 0u, 0u, 0u};
-        const bf16x8 u01 = as_bf16x8(k < p.rank ? ld16(urow + p.ucol[seg[0]]) : zero);
-        const bf16x8 u23 = as_bf16x8(k < p.rank ? ld16(urow + p.ucol[seg[2]]) : zero);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) acc[i][j] = mfma32(lbf[i], i < 2 ? u01 : u23, acc[i][j]);
-      }
-    }
-  }
-
   constexpr int KSTEPS = BK / 16;
   constexpr int NMM = 4 * NJ, NDS = 4 + NJ;
-  constexpr int NMM4 = NMM;
   auto frag = [&](int stage, int s, bf16x8 (&fa)[4], bf16x8 (&fb)[NJ]) {
     const bf16 *sx = lds_x + stage * BM * BK;
     const bf16 *sw = lds_w + stage * BN * BK;
@@ -246,70 +273,6 @@ __global__ __launch_bounds__(64 * WAVES, 1) void gemm_bf16_kernel(const GemmPara
 #pragma unroll
       for (int j = 0; j < NJ; ++j) acc[i][j] = mfma32(fa[i], fb[j], acc[i][j]);
   };
-  if constexpr (WAVES == 4) {
-    // One wave per SIMD: no second wave covers a stall, so fragments are read
-    // two k-steps ahead of their MFMAs (one register set per k-step of a
-    // slice).  The slice barrier sits after k-step 1: by then this wave has
-    // read all of slice kt (its k-steps 2 and 3 were read during k-steps 0
-    // and 1), so the stage can take slice kt+2, and slice kt+1 (issued one
-    // slice earlier) has landed for the reads made during k-steps 2 and 3.
-    static_assert(BK == 64 && STAGES == 2, "two stages of 64-wide slices");
-    bf16x8 fa[4][4], fb[4][NJ];
-    // per k-step region: 16 MFMAs; the first 8 each followed by one LDS read
-    // and, when refilling, one global->LDS load
-    auto sched = [&](auto n_vmem) {
-      constexpr int NV = decltype(n_vmem)::value;
-#pragma unroll
-      for (int i = 0; i < NMM4; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        if (i < 4 + NJ) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-        if (i < NV) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
-      }
-    };
-    dma(kb * BK, 0);
-    dma(min(kb + 1, ke - 1) * BK, 1);
-    wait_vm<DMA_PER_SLICE>();
-    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-    frag(0, 0, fa[0], fb[0]);
-    frag(0, 1, fa[1], fb[1]);
-    for (int kt = kb; kt < ke; ++kt) {
-      const int st = (kt - kb) & 1;
-      __builtin_amdgcn_sched_barrier(0);
-      frag(st, 2, fa[2], fb[2]);
-      mm(fa[0], fb[0]);
-      sched(std::integral_constant<int, 0>());
-      __builtin_amdgcn_sched_barrier(0);
-      frag(st, 3, fa[3], fb[3]);
-      mm(fa[1], fb[1]);
-      sched(std::integral_constant<int, 0>());
-      __builtin_amdgcn_sched_barrier(0);
-      wait_vm<0>();
-      asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-      __builtin_amdgcn_sched_barrier(0);
-      const int kn = min(kt + 2, ke - 1) * BK;  // clamped: every slice issues the same loads
-      dma_part(kn, st, std::integral_constant<int, 0>(), std::integral_constant<int, BLK / 2>());
-      frag(st ^ 1, 0, fa[0], fb[0]);
-      mm(fa[2], fb[2]);
-      sched(std::integral_constant<int, BLK>());
-      __builtin_amdgcn_sched_barrier(0);
-      dma_part(kn, st, std::integral_constant<int, BLK / 2>(), std::integral_constant<int, BLK>());
-      frag(st ^ 1, 1, fa[1], fb[1]);
-      mm(fa[3], fb[3]);
-      sched(std::integral_constant<int, BLK>());
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    wait_vm<0>();
-  } else {
-  // Ring of STAGES slices.  The prologue puts slices 0..STAGES-1 in flight.
-  // Each k-step is one scheduling region: its MFMAs with the next step's
-  // fragment reads interleaved one by one (the MFMAs use fragments read one
-  // region earlier).  The last k-step of a slice follows the slice's single
-  // barrier: wait for slice kt+1 (own DMA; later slices may stay in flight),
-  // a bare barrier that publishes every wave's part and retires all reads of
-  // slice kt, then the refill of that stage with slice kt+STAGES (clamped to
-  // the last slice near the end, so every slice issues the same number of
-  // loads), interleaved with the MFMAs and with slice kt+1's first reads.
-
   auto interleave = [&](auto n_vmem) {
     constexpr int NV = decltype(n_vmem)::value;
 #pragma unroll
@@ -319,14 +282,21 @@ __global__ __launch_bounds__(64 * WAVES, 1) void gemm_bf16_kernel(const GemmPara
       if (i < NDS) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
     }
   };
-#pragma unroll
-  for (int s = 0; s < STAGES; ++s) dma(min(kb + s, ke - 1) * BK, s);
-  wait_vm<(STAGES - 1) * DMA_PER_SLICE>();
-  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+
+  // Ring of STAGES slices.  Each k-step is one scheduling region: its MFMAs
+  // with the next step's fragment reads interleaved one by one (the MFMAs use
+  // fragments read one region earlier).  The last k-step of a slice follows
+  // the slice's single barrier: wait for slice kt+1 (own DMA; later slices
+  // may stay in flight), a bare barrier that publishes every wave's part and
+  // retires all reads of slice kt, then the refill of that stage with the
+  // cursor's slice, interleaved with the MFMAs and with slice kt+1's first
+  // reads.  The last slice of an item defers its refill and the next item's
+  // first reads until after the epilogue, so the epilogue's own loads do not
+  // wait behind that refill.
   bf16x8 a0[4], b0[NJ], a1[4], b1[NJ];
-  frag(0, 0, a0, b0);
   int st = 0;
-  for (int kt = kb; kt < ke; ++kt) {
+  auto slice = [&](auto is_last) {
+    constexpr bool LAST = decltype(is_last)::value;
     const int nst = st + 1 == STAGES ? 0 : st + 1;
 #pragma unroll
     for (int s = 0; s + 1 < KSTEPS; ++s) {
@@ -341,153 +311,271 @@ __global__ __launch_bounds__(64 * WAVES, 1) void gemm_bf16_kernel(const GemmPara
       interleave(std::integral_constant<int, 0>());
       __builtin_amdgcn_sched_barrier(0);
     }
-    // also after the last slice (stage nst then holds a clamped copy): the loop
-    // body stays one basic block per region
     wait_vm<(STAGES - 2) * DMA_PER_SLICE>();
     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
     __builtin_amdgcn_sched_barrier(0);
-    dma(min(kt + STAGES, ke - 1) * BK, st);
-    frag(nst, 0, a0, b0);
+    if constexpr (!LAST) {
+      produce(st);
+      frag(nst, 0, a0, b0);
+    }
     mm(a1, b1);  // KSTEPS is even: the last k-step of a slice uses (a1, b1)
-    interleave(std::integral_constant<int, DMA_PER_SLICE>());
+    interleave(std::integral_constant<int, LAST ? 0 : DMA_PER_SLICE>());
     __builtin_amdgcn_sched_barrier(0);
-    st = nst;
-  }
-  wait_vm<0>();  // the clamped refills of the last slices
+    if constexpr (!LAST) {
+      advance();
+      st = nst;
+    }
+  };
+
+  if (mine > 0) {
+    producer_setup(0);
+#pragma unroll
+    for (int s = 0; s < STAGES; ++s) {
+      produce(s);
+      advance();
+    }
+    wait_vm<(STAGES - 1) * DMA_PER_SLICE>();
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    frag(0, 0, a0, b0);
   }
 
-  // ---- epilogues
-  if (EPI == EPI_RESID && part >= 0) {  // fp32 partial of a K-part, [256 tokens][256 features]
-    float *pp = p.split_part + (int64_t)(w - p.split_first) * BM * BN;
+  int run_tm = -1, run_slot = -1, n_run = 0;
+  for (int i = 0; i < mine; ++i) {
+    const WorkItem it = work_item(sc, b, i);
+    const int m0 = it.tm * BM, n0 = it.tn * BN;
+    const int part = it.part;
+
+    for (int kt = it.kb; kt + 1 < it.ke; ++kt) slice(std::false_type());
+    slice(std::true_type());
+
+    // ---- low-rank delta: acc += U[token, ucol_s + k] * lb_s[feature, k] (K-part 0 only)
+    if (p.U && part <= 0) {
+      int seg[4], frow[4];
 #pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-      const int ml = wm * WTM + 32 * j + l32;
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int ii = 0; ii < 4; ++ii) {
+        const int r = min(n0 + wn * 128 + 32 * ii + l32, p.N - 1);
+        seg[ii] = segment_of<EPI>(p, r, frow[ii]);
+      }
+      for (int kk = 0; kk < p.kpad; kk += 16) {
+        const int k = kk + 8 * g;
+        bf16x8 lbf[4];
 #pragma unroll
         for (int ii = 0; ii < 4; ++ii) {
-          const int nl = wn * 128 + 32 * i + 8 * ii + 4 * g;
-          *reinterpret_cast<f32x4 *>(pp + ml * BN + nl) =
-              f32x4{acc[i][j][ii * 4], acc[i][j][ii * 4 + 1], acc[i][j][ii * 4 + 2], acc[i][j][ii * 4 + 3]};
+          u32x4 v = {0u, 0u, 0u, 0u};
+          const bf16 *lb = p.lb[seg[ii]];
+          if (lb && k < p.rank) v = ld16(lb + (int64_t)frow[ii] * p.rank + k);
+          lbf[ii] = as_bf16x8(v);
         }
-    }
-  } else if (EPI == EPI_RESID) {
 #pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-      const int m = m0 + wm * WTM + 32 * j + l32;
-      if (m >= p.M) continue;
+        for (int j = 0; j < NJ; ++j) {
+          const int m = min(m0 + wm * WTM + 32 * j + l32, p.M - 1);
+          const bf16 *urow = p.U + (int64_t)m * p.ldu + k;
+          // segments used by this wave: blocks 0,1 and 2,3 may differ (EPI_SWIGLU);
+          // U columns past the rank stay unread (the factor side is zero there,
+          // and they may lie past the row or the buffer)
+          const u32x4 zero = {0u, 0u, 0u, 0u};
+          const bf16x8 u01 = as_bf16x8(k < p.rank ? ld16(urow + p.ucol[seg[0]]) : zero);
+          const bf16x8 u23 = as_bf16x8(k < p.rank ? ld16(urow + p.ucol[seg[2]]) : zero);
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int ii = 0; ii < 4; ++ii) {
-          const int n = n0 + wn * 128 + 32 * i + 8 * ii + 4 * g;
-          if (n >= p.N) continue;
-          float *rp = p.resid + (int64_t)m * p.ldr + n;
-          f32x4 r = p.resid_overwrite ? f32x4{0.f, 0.f, 0.f, 0.f} : *reinterpret_cast<f32x4 *>(rp);
-#pragma unroll
-          for (int jj = 0; jj < 4; ++jj) r[jj] += acc[i][j][ii * 4 + jj];
-          *reinterpret_cast<f32x4 *>(rp) = r;
-          if (p.resid_out) st8(p.resid_out + (int64_t)m * p.ldr + n, pack_bf16x4(r[0], r[1], r[2], r[3]));
+          for (int ii = 0; ii < 4; ++ii) acc[ii][j] = mfma32(lbf[ii], ii < 2 ? u01 : u23, acc[ii][j]);
         }
+      }
     }
-  } else if (EPI == EPI_SWIGLU) {
-    const int fbase = (n0 + wn * 128) / 2;
+
+    // ---- epilogues
+    if (EPI == EPI_RESID && part >= 0) {  // fp32 partial of a K-part, [256 tokens][256 features]
+      float *pp = p.split_part + (int64_t)(it.w - sc.split_first) * BM * BN;
 #pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-      const int m = m0 + wm * WTM + 32 * j + l32;
-      if (m >= p.M) continue;
+      for (int j = 0; j < NJ; ++j) {
+        float *pr = pp + (wm * WTM + 32 * j + l32) * BN + wn * 128 + 4 * g;
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+        for (int ii = 0; ii < 4; ++ii)
 #pragma unroll
-        for (int ii = 0; ii < 4; ++ii) {
-          const int f = fbase + 32 * i + 8 * ii + 4 * g;
-          if (f >= p.d_ffn) continue;
-          float o[4];
+          for (int q = 0; q < 4; ++q)
+            *reinterpret_cast<f32x4 *>(pr + 32 * ii + 8 * q) = f32x4{acc[ii][j][q * 4], acc[ii][j][q * 4 + 1],
+                                                                     acc[ii][j][q * 4 + 2], acc[ii][j][q * 4 + 3]};
+      }
+    } else if (EPI == EPI_RESID) {
 #pragma unroll
-          for (int jj = 0; jj < 4; ++jj) {
-            const float gt = acc[i][j][ii * 4 + jj], up = acc[i + 2][j][ii * 4 + jj];
-            o[jj] = gt / (1.0f + __expf(-gt)) * up;
+      for (int j = 0; j < NJ; ++j) {
+        const int m = m0 + wm * WTM + 32 * j + l32;
+        if (m >= p.M) continue;
+#pragma unroll
+        for (int ii = 0; ii < 4; ++ii)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int n = n0 + wn * 128 + 32 * ii + 8 * q + 4 * g;
+            if (n >= p.N) continue;
+            float *rp = p.resid + (int64_t)m * p.ldr + n;
+            f32x4 r = p.resid_overwrite ? f32x4{0.f, 0.f, 0.f, 0.f} : *reinterpret_cast<f32x4 *>(rp);
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) r[jj] += acc[ii][j][q * 4 + jj];
+            *reinterpret_cast<f32x4 *>(rp) = r;
+            if (p.resid_out) st8(p.resid_out + (int64_t)m * p.ldr + n, pack_bf16x4(r[0], r[1], r[2], r[3]));
           }
-          st8(p.act + (int64_t)m * p.d_ffn + f, pack_bf16x4(o[0], o[1], o[2], o[3]));
+      }
+    } else if (EPI == EPI_SWIGLU) {
+      const int fbase = (n0 + wn * 128) / 2;
+      // fused adapter sums: this run's slot (a new run starts on a new token tile)
+      if (dn_on) {
+        bool head = false;
+        if (it.tm != run_tm) {
+          if (run_tm >= 0) dn_flush(run_tm, run_slot);
+          run_tm = it.tm;
+          run_slot = b * p.dn_runs + n_run++;
+          head = true;
         }
-    }
-  } else {  // EPI_QKV
-    constexpr int BPH = HD / 32;          // 32-row blocks per head
-    constexpr int HPW = 128 / HD;         // heads per wave
-    const int fb = n0 + wn * 128;         // first tile-space row of this wave (head aligned)
-    int local;
-    const int sg = segment_of<EPI>(p, fb, local);
-    const int head0 = local / HD;
-    const bf16 *bias = p.bias[sg];
+        // every tile records whether it opens a run (slot + 1) or not (0)
+        if (tid == 0) p.dn_head[it.tm * sc.tiles_n + it.tn] = head ? run_slot + 1 : 0;
+      }
 #pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-      const int m = m0 + wm * WTM + 32 * j + l32;
-      if (m >= p.M || fb >= p.N) continue;
-      int64_t prow[HPW];
+      for (int j = 0; j < NJ; ++j) {
+        const int m = m0 + wm * WTM + 32 * j + l32;
+        u32x2 packed[2][4];
 #pragma unroll
-      for (int hh = 0; hh < HPW; ++hh) prow[hh] = sg ? paged_row(p.kv, p.pos0 + m, head0 + hh, HD) : 0;
-      const float2 *cs = p.rope_cs + (int64_t)(p.pos0 + m) * (HD / 2);
+        for (int ii = 0; ii < 2; ++ii)
 #pragma unroll
-      for (int hh = 0; hh < HPW; ++hh)
-#pragma unroll
-        for (int i = 0; i < BPH / 2; ++i)
-#pragma unroll
-          for (int ii = 0; ii < 4; ++ii) {
-            const int f = 32 * i + 8 * ii + 4 * g;  // in-head index of the first of 4 rows (< HD/2)
-            const int b1 = hh * BPH + i, b2 = b1 + BPH / 2;
-            float x1[4], x2[4];
+          for (int q = 0; q < 4; ++q) {
+            float o[4];
 #pragma unroll
             for (int jj = 0; jj < 4; ++jj) {
-              x1[jj] = acc[b1][j][ii * 4 + jj];
-              x2[jj] = acc[b2][j][ii * 4 + jj];
+              const float gt = acc[ii][j][q * 4 + jj], up = acc[ii + 2][j][q * 4 + jj];
+              o[jj] = gt * __builtin_amdgcn_rcpf(1.0f + __expf(-gt)) * up;
             }
-            if (bias) {
-              const bf16 *bp = bias + (head0 + hh) * HD + f;
-#pragma unroll
-              for (int jj = 0; jj < 4; ++jj) {
-                x1[jj] += bf2f(bp[jj]);
-                x2[jj] += bf2f(bp[jj + HD / 2]);
-              }
-            }
-            if (sg < 2) {  // rotate Q and K
-#pragma unroll
-              for (int jj = 0; jj < 4; ++jj) {
-                const float2 c = cs[f + jj];
-                const float y1 = x1[jj] * c.x - x2[jj] * c.y;
-                const float y2 = x2[jj] * c.x + x1[jj] * c.y;
-                x1[jj] = y1;
-                x2[jj] = y2;
-              }
-            }
-            bf16 *dst;
-            if (sg == 0) {
-              dst = p.q_out + (int64_t)m * p.dq + (head0 + hh) * HD;
-            } else {
-              if (prow[hh] < 0) continue;
-              dst = (bf16 *)(sg == 1 ? p.kv.k : p.kv.v) + prow[hh];
-            }
-            st8(dst + f, pack_bf16x4(x1[0], x1[1], x1[2], x1[3]));
-            st8(dst + f + HD / 2, pack_bf16x4(x2[0], x2[1], x2[2], x2[3]));
+            packed[ii][q] = pack_bf16x4(o[0], o[1], o[2], o[3]);
+            const int f = fbase + 32 * ii + 8 * q + 4 * g;
+            if (m < p.M && f < p.d_ffn) st8(p.act + (int64_t)m * p.d_ffn + f, packed[ii][q]);
           }
+        if (dn_on && fbase < p.d_ffn) {
+          // D[rank, token] += A_down[rank, f] act[token, f] over this wave's 64
+          // features, 16 at a time.  The B operand is a lane's own stored act
+          // values: k-slot e of k-step (ii, h) is feature
+          // fbase + 32 ii + 16 h + 8 (e / 4) + 4 g + e % 4, and the factor rows
+          // (rank = l32; rows past the rank are zero) are read in that order.
+          f32x16 ud;
+#pragma unroll
+          for (int v = 0; v < 16; ++v) ud[v] = 0.f;
+#pragma unroll
+          for (int ii = 0; ii < 2; ++ii)
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+              const int f0 = fbase + 32 * ii + 16 * h + 4 * g;
+              u32x4 av = {0u, 0u, 0u, 0u};
+              if (l32 < p.dn_rank) {
+                const bf16 *ar = p.dn_a + (int64_t)l32 * p.d_ffn + f0;
+                const u32x2 lo = ld8(ar), hi = ld8(ar + 8);
+                av = u32x4{lo[0], lo[1], hi[0], hi[1]};
+              }
+              const u32x4 bv = {packed[ii][2 * h][0], packed[ii][2 * h][1], packed[ii][2 * h + 1][0],
+                                packed[ii][2 * h + 1][1]};
+              ud = mfma32(as_bf16x8(av), as_bf16x8(bv), ud);
+            }
+          // ranks 8 (v / 4) + 4 g + v % 4 for v < 8 (rows 16..31 are padding)
+          float *d = dn_lds + (wn * BM + wm * WTM + 32 * j + l32) * DN_RANK + 4 * g;
+          f32x4 s0 = *reinterpret_cast<f32x4 *>(d), s1 = *reinterpret_cast<f32x4 *>(d + 8);
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            s0[v] += ud[v];
+            s1[v] += ud[4 + v];
+          }
+          *reinterpret_cast<f32x4 *>(d) = s0;
+          *reinterpret_cast<f32x4 *>(d + 8) = s1;
+        }
+      }
+    } else {  // EPI_QKV
+      constexpr int BPH = HD / 32;          // 32-row blocks per head
+      constexpr int HPW = 128 / HD;         // heads per wave
+      const int fb = n0 + wn * 128;         // first tile-space row of this wave (head aligned)
+      int local;
+      const int sg = segment_of<EPI>(p, fb, local);
+      const int head0 = local / HD;
+      const bf16 *bias = p.bias[sg];
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) {
+        const int m = m0 + wm * WTM + 32 * j + l32;
+        if (m >= p.M || fb >= p.N) continue;
+        int64_t prow[HPW];
+#pragma unroll
+        for (int hh = 0; hh < HPW; ++hh) prow[hh] = sg ? paged_row(p.kv, p.pos0 + m, head0 + hh, HD) : 0;
+        const float2 *cs = p.rope_cs + (int64_t)(p.pos0 + m) * (HD / 2);
+#pragma unroll
+        for (int hh = 0; hh < HPW; ++hh)
+#pragma unroll
+          for (int ii = 0; ii < BPH / 2; ++ii)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const int f = 32 * ii + 8 * q + 4 * g;  // in-head index of the first of 4 rows (< HD/2)
+              const int b1 = hh * BPH + ii, b2 = b1 + BPH / 2;
+              float x1[4], x2[4];
+#pragma unroll
+              for (int jj = 0; jj < 4; ++jj) {
+                x1[jj] = acc[b1][j][q * 4 + jj];
+                x2[jj] = acc[b2][j][q * 4 + jj];
+              }
+              if (bias) {
+                const bf16 *bp = bias + (head0 + hh) * HD + f;
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj) {
+                  x1[jj] += bf2f(bp[jj]);
+                  x2[jj] += bf2f(bp[jj + HD / 2]);
+                }
+              }
+              if (sg < 2) {  // rotate Q and K
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj) {
+                  const float2 c = cs[f + jj];
+                  const float y1 = x1[jj] * c.x - x2[jj] * c.y;
+                  const float y2 = x2[jj] * c.x + x1[jj] * c.y;
+                  x1[jj] = y1;
+                  x2[jj] = y2;
+                }
+              }
+              bf16 *dst;
+              if (sg == 0) {
+                dst = p.q_out + (int64_t)m * p.dq + (head0 + hh) * HD;
+              } else {
+                if (prow[hh] < 0) continue;
+                dst = (bf16 *)(sg == 1 ? p.kv.k : p.kv.v) + prow[hh];
+              }
+              st8(dst + f, pack_bf16x4(x1[0], x1[1], x1[2], x1[3]));
+              st8(dst + f + HD / 2, pack_bf16x4(x2[0], x2[1], x2[2], x2[3]));
+            }
+      }
     }
+
+    // the deferred refill (the next item's second slice) and the next item's
+    // first fragments, then a fresh accumulator
+    if (i + 1 < mine) {
+      produce(st);
+      advance();
+      st = st + 1 == STAGES ? 0 : st + 1;
+      frag(st, 0, a0, b0);
+    }
+#pragma unroll
+    for (int ii = 0; ii < 4; ++ii)
+#pragma unroll
+      for (int j = 0; j < NJ; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[ii][j][v] = 0.f;
   }
+  if (dn_on && run_tm >= 0) dn_flush(run_tm, run_slot);
+  wait_vm<0>();  // refills nobody consumes must land before the workgroup ends
 }
 
 // resid[m, n] (+)= sum over the K-parts of a split tile, in part order; one
 // thread per 4 features.
-__global__ __launch_bounds__(256) void split_reduce_kernel(const GemmParams p) {
-  const int tiles_m = (p.M + BM - 1) / BM, tiles_n = (p.N + BN - 1) / BN;
+__global__ __launch_bounds__(256) void split_reduce_kernel(const GemmParams p, const Sched sc) {
   const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;  // over split tiles x 256 x 64
   const int ti = (int)(idx / (BM * BN / 4));
   const int e = (int)(idx % (BM * BN / 4));
   const int ml = e / (BN / 4), nl = 4 * (e % (BN / 4));
   int tm, tn;
-  tile_coords(p.split_first + ti, tiles_m, tiles_n, tm, tn);
+  tile_coords(sc.split_first + ti, sc.tiles_m, sc.tiles_n, tm, tn);
   const int m = tm * BM + ml, n = tn * BN + nl;
   if (m >= p.M || n >= p.N) return;
-  const float *pp = p.split_part + (int64_t)ti * p.split_s * BM * BN + ml * BN + nl;
+  const float *pp = p.split_part + (int64_t)ti * sc.split_s * BM * BN + ml * BN + nl;
   f32x4 v = *reinterpret_cast<const f32x4 *>(pp);
-  for (int sp = 1; sp < p.split_s; ++sp) v += *reinterpret_cast<const f32x4 *>(pp + (int64_t)sp * BM * BN);
+  for (int sp = 1; sp < sc.split_s; ++sp) v += *reinterpret_cast<const f32x4 *>(pp + (int64_t)sp * BM * BN);
   float *rp = p.resid + (int64_t)m * p.ldr + n;
   f32x4 r = p.resid_overwrite ? f32x4{0.f, 0.f, 0.f, 0.f} : *reinterpret_cast<f32x4 *>(rp);
   r += v;
@@ -495,16 +583,42 @@ __global__ __launch_bounds__(256) void split_reduce_kernel(const GemmParams p) {
   if (p.resid_out) st8(p.resid_out + (int64_t)m * p.ldr + n, pack_bf16x4(r[0], r[1], r[2], r[3]));
 }
 
-template <int EPI, int HD, int WAVES>
-hipError_t go(hipStream_t s, const GemmParams &p0) {
-  const int tiles = ((p0.M + BM - 1) / BM) * ((p0.N + BN - 1) / BN);
-  GemmParams p = p0;
-  p.split_first = tiles;
-  p.split_s = 1;
-  if (EPI == EPI_RESID && p.split_part && p.n_cu > 0) {
+// U[m, ucol + r] = bf16(scale * sum of the fused down-projection adapter sums
+// of token m): over the runs that cover m's token tile in increasing order of
+// their first tile, then over the two feature halves.  One thread per 4 ranks.
+__global__ __launch_bounds__(256) void dn_sum_kernel(const GemmParams p, const Sched sc, bf16 *U, int ldu, int ucol,
+                                                     float scale) {
+  const int idx = blockIdx.x * 256 + threadIdx.x;
+  const int m = idx / (DN_RANK / 4), r = 4 * (idx % (DN_RANK / 4));
+  if (m >= p.M || r >= p.dn_rank) return;
+  const int tm = m / BM, ml = m % BM;
+  const int *head = p.dn_head + tm * sc.tiles_n;
+  f32x4 v = {0.f, 0.f, 0.f, 0.f};
+  for (int tn = 0; tn < sc.tiles_n; ++tn) {
+    const int h = head[tn];
+    if (!h) continue;
+#pragma unroll
+    for (int wn = 0; wn < 2; ++wn)
+      v += *reinterpret_cast<const f32x4 *>(p.dn_part + (((int64_t)(h - 1) * 2 + wn) * BM + ml) * DN_RANK + r);
+  }
+  bf16 *u = U + (int64_t)m * ldu + ucol + r;
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+    if (r + q < p.dn_rank) u[q] = f2bf(v[q] * scale);
+}
+
+Sched schedule(GemmEpi epi, const GemmParams &p) {
+  Sched sc{};
+  sc.tiles_m = (p.M + BM - 1) / BM;
+  sc.tiles_n = (p.N + BN - 1) / BN;
+  sc.nk = p.K / BK;
+  const int tiles = sc.tiles_m * sc.tiles_n;
+  sc.split_first = tiles;
+  sc.split_s = 1;
+  if (epi == EPI_RESID && p.split_part && p.n_cu > 0) {
     // a last wave at most half full: split its tiles (or all tiles, when there
     // are fewer than compute units) into K-parts of at least 8 slices
-    const int nk = p.K / BK, r = tiles % p.n_cu;
+    const int r = tiles % p.n_cu;
     int first = tiles, sp = 1;
     if (tiles < p.n_cu) {
       first = 0;
@@ -513,14 +627,39 @@ hipError_t go(hipStream_t s, const GemmParams &p0) {
       first = tiles - r;
       sp = 2;
     }
-    sp = std::min(sp, std::min(8, nk / 8));
+    sp = std::min(sp, std::min(8, sc.nk / 8));
     if (sp >= 2 && (int64_t)(tiles - first) * sp * BM * BN <= p.split_cap) {
-      p.split_first = first;
-      p.split_s = sp;
+      sc.split_first = first;
+      sc.split_s = sp;
     }
   }
-  const int grid = p.split_first + (tiles - p.split_first) * p.split_s;
-  const size_t lds = (size_t)STAGES * (BM + BN) * BK * sizeof(bf16);
+  sc.n_items = sc.split_first + (tiles - sc.split_first) * sc.split_s;
+  sc.grid = p.n_cu > 0 ? std::min(sc.n_items, p.n_cu) : sc.n_items;
+  // K-parts sit at the end of every workgroup's list when the last round is
+  // split; with a short K range (where the residual epilogue is a large share
+  // of an item) odd workgroups take theirs first, so that half of the
+  // workgroups reach each residual epilogue at another time
+  sc.stagger = sc.split_s > 1 && sc.split_first % sc.grid == 0 && (sc.n_items - sc.split_first) == sc.grid &&
+               sc.nk <= 128;
+  return sc;
+}
+
+template <int EPI, int HD>
+hipError_t go(hipStream_t s, const GemmParams &p0, bool *dn_done) {
+  GemmParams p = p0;
+  const Sched sc = schedule((GemmEpi)EPI, p);
+  p.split_first = sc.split_first;
+  p.split_s = sc.split_s;
+  bool dn = false;
+  if (EPI == EPI_SWIGLU && p.dn_a && p.dn_part && p.dn_head && p.dn_rank > 0 && p.dn_rank <= DN_RANK &&
+      p.dn_runs > 0 && STAGE_BYTES + DN_BYTES <= 160 * 1024) {
+    int runs = 0;
+    for (int b = 0; b < sc.grid && runs <= p.dn_runs; ++b) runs = std::max(runs, n_runs(sc, b));
+    dn = runs <= p.dn_runs;
+  }
+  if (!dn) p.dn_a = nullptr;
+  if (dn_done) *dn_done = dn;
+  const size_t lds = (size_t)STAGE_BYTES + (dn ? DN_BYTES : 0);
   // the dynamic-LDS limit is raised once per device (bit d of attr_set)
   static std::atomic<uint64_t> attr_set{0};
   int dev = 0;
@@ -528,34 +667,42 @@ hipError_t go(hipStream_t s, const GemmParams &p0) {
   if (e != hipSuccess) return e;
   const uint64_t bit = dev < 64 ? (uint64_t)1 << dev : 0;
   if (!bit || !(attr_set.load() & bit)) {
-    e = hipFuncSetAttribute((const void *)gemm_bf16_kernel<EPI, HD, WAVES>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                            (int)lds);
+    e = hipFuncSetAttribute((const void *)gemm_bf16_kernel<EPI, HD>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            STAGE_BYTES + (EPI == EPI_SWIGLU ? DN_BYTES : 0));
     if (e != hipSuccess) return e;
     attr_set.fetch_or(bit);
   }
-  hipLaunchKernelGGL((gemm_bf16_kernel<EPI, HD, WAVES>), dim3(grid), dim3(64 * WAVES), lds, s, p);
-  if (p.split_s > 1) {
-    const hipError_t e = hipGetLastError();
+  hipLaunchKernelGGL((gemm_bf16_kernel<EPI, HD>), dim3(sc.grid), dim3(64 * WAVES), lds, s, p, sc);
+  if (sc.split_s > 1) {
+    e = hipGetLastError();
     if (e != hipSuccess) return e;
-    const int64_t n = (int64_t)(tiles - p.split_first) * BM * BN / 4;
-    hipLaunchKernelGGL(split_reduce_kernel, dim3((unsigned)(n / 256)), dim3(256), 0, s, p);
+    const int64_t n = (int64_t)(sc.tiles_m * sc.tiles_n - sc.split_first) * BM * BN / 4;
+    hipLaunchKernelGGL(split_reduce_kernel, dim3((unsigned)(n / 256)), dim3(256), 0, s, p, sc);
   }
   return hipGetLastError();
 }
 
 }  // namespace
 
-hipError_t launch_gemm_bf16(hipStream_t s, GemmEpi epi, int hd, const GemmParams &p) {
-  constexpr int W = CRF_GEMM_WAVES;
+hipError_t launch_gemm_bf16(hipStream_t s, GemmEpi epi, int hd, const GemmParams &p, bool *dn_done) {
+  if (dn_done) *dn_done = false;
   if (p.M <= 0 || p.N <= 0) return hipSuccess;
   if (p.K % BK) return hipErrorInvalidValue;
   if ((int64_t)p.M * p.ldx * 2 >= (int64_t)CRF_OOB) return hipErrorInvalidValue;  // X must fit one buffer resource
   switch (epi) {
-    case EPI_RESID: return go<EPI_RESID, 128, W>(s, p);
-    case EPI_SWIGLU: return go<EPI_SWIGLU, 128, W>(s, p);
-    case EPI_QKV: return hd == 64 ? go<EPI_QKV, 64, W>(s, p) : go<EPI_QKV, 128, W>(s, p);
+    case EPI_RESID: return go<EPI_RESID, 128>(s, p, nullptr);
+    case EPI_SWIGLU: return go<EPI_SWIGLU, 128>(s, p, dn_done);
+    case EPI_QKV: return hd == 64 ? go<EPI_QKV, 64>(s, p, nullptr) : go<EPI_QKV, 128>(s, p, nullptr);
   }
   return hipErrorInvalidValue;
+}
+
+hipError_t launch_gemm_dn_sum(hipStream_t s, const GemmParams &p, bf16 *U, int ldu, int ucol, float scale) {
+  if (p.M <= 0) return hipSuccess;
+  const Sched sc = schedule(EPI_SWIGLU, p);
+  const int threads = p.M * (DN_RANK / 4);
+  hipLaunchKernelGGL(dn_sum_kernel, dim3((threads + 255) / 256), dim3(256), 0, s, p, sc, U, ldu, ucol, scale);
+  return hipGetLastError();
 }
 
 }  // namespace crf

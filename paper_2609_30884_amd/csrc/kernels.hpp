@@ -95,8 +95,25 @@ struct GemmParams {
   int64_t split_cap;
   int n_cu;
   int split_first, split_s;
+  // EPI_SWIGLU: the down projection's adapter down-projection fused into the
+  // epilogue (rank <= 16): dn_a = A_down [dn_rank, d_ffn].  Each workgroup sums
+  // act . A_down^T over the features of consecutive items on one token tile (a
+  // run) and leaves the sums in dn_part slot b * dn_runs + run ([slot][2][256][16]
+  // fp32); dn_head[tm * tiles_n + tn] = slot + 1 for the first tile of a run,
+  // else 0.  launch_gemm_dn_sum then forms U.
+  const bf16 *dn_a;
+  int dn_rank;
+  float *dn_part;
+  int *dn_head;
+  int dn_runs;
 };
-hipError_t launch_gemm_bf16(hipStream_t s, GemmEpi epi, int hd, const GemmParams &p);
+// Persistent over at most n_cu workgroups (n_cu > 0).  *dn_done (nullable)
+// reports whether the fused down-projection sums were produced (they are
+// skipped when a workgroup would need more than dn_runs runs).
+hipError_t launch_gemm_bf16(hipStream_t s, GemmEpi epi, int hd, const GemmParams &p, bool *dn_done = nullptr);
+// U[m, ucol + r] = bf16(scale * sum of the fused sums) for r < dn_rank, after
+// launch_gemm_bf16(EPI_SWIGLU) reported *dn_done with the same parameters.
+hipError_t launch_gemm_dn_sum(hipStream_t s, const GemmParams &p, bf16 *U, int ldu, int ucol, float scale);
 // The same projections for M <= 16 token rows (weight-streaming bound).
 hipError_t launch_gemm_skinny_bf16(hipStream_t s, GemmEpi epi, int hd, const GemmParams &p);
 

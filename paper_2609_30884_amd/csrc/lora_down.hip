@@ -25,16 +25,16 @@ struct LdArgs {
   float *part;  // non-null: fp32 partial sums [grid.y][16][n_targets * rank_pad], unscaled
 };
 
-// Workgroup: TB blocks of 16 tokens, 4 waves splitting K (wave w takes k-steps
-// w, w+4, ...).  Per k-step of 32: D[j, token] += A_t[j, k..k+32] .
+// Workgroup: TB blocks of 16 tokens, NW waves splitting K (wave w takes k-steps
+// w, w+NW, ...).  Per k-step of 32: D[j, token] += A_t[j, k..k+32] .
 // X[token, k..k+32] on the 16x16x32 MFMA, one MFMA per (16-row block of the
 // concatenated factors, token block): the factors are read once per TB*16
 // tokens.  The loads of UNROLL k-steps are issued before their MFMAs so enough
 // bytes are in flight to keep HBM busy; the factors (a few hundred KB) stay in
 // L2.
-template <int NB, int UNROLL, int TB>
-__global__ __launch_bounds__(256) void lora_down_kernel(LdArgs a) {
-  __shared__ f32x4 red[4][NB * TB][64];
+template <int NB, int UNROLL, int TB, int NW = 4>
+__global__ __launch_bounds__(64 * NW) void lora_down_kernel(LdArgs a) {
+  __shared__ f32x4 red[NW][NB * TB][64];
   const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
   const int m0 = blockIdx.x * 16 * TB;
   const int kq = (lane / 16) * 8;
@@ -55,12 +55,12 @@ __global__ __launch_bounds__(256) void lora_down_kernel(LdArgs a) {
 #pragma unroll
     for (int tb = 0; tb < TB; ++tb) acc[b][tb] = f32x4{0.f, 0.f, 0.f, 0.f};
   const int s0 = blockIdx.y * a.spw, s1 = min(a.K / 32, s0 + a.spw);
-  for (int st = s0 + wave; st < s1; st += 4 * UNROLL) {
+  for (int st = s0 + wave; st < s1; st += NW * UNROLL) {
     bf16x8 xb[UNROLL][TB], ab[UNROLL][NB];
 #pragma unroll
     for (int u = 0; u < UNROLL; ++u) {
-      if (st + 4 * u < s1) {  // wave-uniform
-        const int k = (st + 4 * u) * 32;
+      if (st + NW * u < s1) {  // wave-uniform
+        const int k = (st + NW * u) * 32;
 #pragma unroll
         for (int tb = 0; tb < TB; ++tb) xb[u][tb] = as_bf16x8(ld16(xrow[tb] + k));
 #pragma unroll
@@ -71,7 +71,7 @@ __global__ __launch_bounds__(256) void lora_down_kernel(LdArgs a) {
     __builtin_amdgcn_sched_barrier(0);  // every load of the batch in flight before the first MFMA
 #pragma unroll
     for (int u = 0; u < UNROLL; ++u)
-      if (st + 4 * u < s1)
+      if (st + NW * u < s1)
 #pragma unroll
         for (int b = 0; b < NB; ++b)
 #pragma unroll
@@ -90,7 +90,7 @@ __global__ __launch_bounds__(256) void lora_down_kernel(LdArgs a) {
   for (int b = 0; b < NB; ++b) {
     f32x4 v = red[0][b * TB + wave][lane];
 #pragma unroll
-    for (int w = 1; w < 4; ++w) v += red[w][b * TB + wave][lane];
+    for (int w = 1; w < NW; ++w) v += red[w][b * TB + wave][lane];
     if (a.part) {  // K split over workgroups: unscaled partial, summed by lora_down_sum_kernel
       const int ncols = a.n_targets * a.rank_pad;
       *reinterpret_cast<f32x4 *>(a.part + ((int64_t)blockIdx.y * 16 + m) * ncols + b * 16 + (lane / 16) * 4) = v;
@@ -145,8 +145,10 @@ void go(hipStream_t s, LdArgs a, float *ws, int64_t ws_floats, LoraSplit *split)
   a.spw = nsteps;
   a.part = nullptr;
   if constexpr (NB <= 4) {
-    if (a.M >= 8192) {  // 64 tokens per workgroup: the factors are read once per 64 tokens
-      hipLaunchKernelGGL((lora_down_kernel<NB, 4, 4>), dim3((a.M + 63) / 64), dim3(256), 0, s, a);
+    if (a.M >= 8192) {
+      // 64 tokens per workgroup (the factors are read once per 64 tokens) and
+      // 8 waves splitting K, so that enough loads are in flight per CU
+      hipLaunchKernelGGL((lora_down_kernel<NB, 4, 4, 8>), dim3((a.M + 63) / 64), dim3(512), 0, s, a);
       return;
     }
   }
