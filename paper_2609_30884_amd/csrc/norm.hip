@@ -70,6 +70,49 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const TX *__restrict__ x, 
   }
 }
 
+// The same with the row held in registers (one pass over HBM): lane l holds
+// elements [512 c + 8 l, 512 c + 8 l + 8) of chunk c < NCH, d <= 512 NCH.  All
+// of a wave's loads are issued before the first use, so a row's bytes are in
+// flight at once.
+template <typename TX, typename TG, typename TY, int NCH>
+__global__ __launch_bounds__(256) void rmsnorm_reg_kernel(const TX *__restrict__ x, const TG *__restrict__ g,
+                                                          TY *__restrict__ y, float *__restrict__ copy_out, int M,
+                                                          int d, float eps) {
+  const int row = blockIdx.x * 4 + threadIdx.x / 64;
+  const int lane = threadIdx.x % 64;
+  if (row >= M) return;
+  const TX *xr = x + (int64_t)row * d;
+  float v[NCH][8];
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    const int k = 512 * c + lane * 8;
+    if (k < d) {
+      load8(xr + k, v[c]);
+    } else {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[c][i] = 0.f;
+    }
+  }
+  float ss = 0.f;
+#pragma unroll
+  for (int c = 0; c < NCH; ++c)
+#pragma unroll
+    for (int i = 0; i < 8; ++i) ss = fmaf(v[c][i], v[c][i], ss);
+  ss = wave_sum(ss);
+  const float r = 1.0f / sqrtf(ss / (float)d + eps);
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    const int k = 512 * c + lane * 8;
+    if (k >= d) continue;
+    if (copy_out) store8(copy_out + (int64_t)row * d + k, v[c]);
+    float gv[8];
+    load8(g + k, gv);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) gv[i] = v[c][i] * r * gv[i];
+    store8(y + (int64_t)row * d + k, gv);
+  }
+}
+
 __global__ void rope_table_kernel(float2 *cs, int T, int hd, double log_theta) {
   const int half = hd / 2;
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -83,8 +126,22 @@ __global__ void rope_table_kernel(float2 *cs, int T, int hd, double log_theta) {
 template <typename TX, typename TG, typename TY>
 hipError_t go(hipStream_t s, const void *x, const void *g, void *y, float *copy_out, int M, int d, float eps) {
   if (M <= 0) return hipSuccess;
-  hipLaunchKernelGGL((rmsnorm_kernel<TX, TG, TY>), dim3((M + 3) / 4), dim3(256), 0, s, (const TX *)x,
-                     (const TG *)g, (TY *)y, copy_out, M, d, eps);
+  const dim3 grid((M + 3) / 4), block(256);
+  const TX *xp = (const TX *)x;
+  const TG *gp = (const TG *)g;
+  TY *yp = (TY *)y;
+  switch ((d + 511) / 512) {
+#define CRF_NORM_CASE(n)                                                                                   \
+  case n:                                                                                                  \
+    hipLaunchKernelGGL((rmsnorm_reg_kernel<TX, TG, TY, n>), grid, block, 0, s, xp, gp, yp, copy_out, M, d, eps); \
+    break;
+    CRF_NORM_CASE(1) CRF_NORM_CASE(2) CRF_NORM_CASE(3) CRF_NORM_CASE(4) CRF_NORM_CASE(5) CRF_NORM_CASE(6)
+    CRF_NORM_CASE(7) CRF_NORM_CASE(8) CRF_NORM_CASE(9) CRF_NORM_CASE(10) CRF_NORM_CASE(11) CRF_NORM_CASE(12)
+    CRF_NORM_CASE(13) CRF_NORM_CASE(14) CRF_NORM_CASE(15) CRF_NORM_CASE(16)
+#undef CRF_NORM_CASE
+    default:  // wider rows: two passes over the row
+      hipLaunchKernelGGL((rmsnorm_kernel<TX, TG, TY>), grid, block, 0, s, xp, gp, yp, copy_out, M, d, eps);
+  }
   return hipGetLastError();
 }
 
