@@ -383,7 +383,7 @@ __global__ __launch_bounds__(64 * WAVES, 1) void gemm_bf16_kernel(const GemmPara
     }
 
     // ---- epilogues
-    if (EPI == EPI_RESID && part >= 0) {  // fp32 partial of a K-part, [256 tokens][256 features]
+    if ((EPI == EPI_RESID || EPI == EPI_QKV) && part >= 0) {  // fp32 partial of a K-part, [256 tokens][256 features]
       float *pp = p.split_part + (int64_t)(it.w - sc.split_first) * BM * BN;
 #pragma unroll
       for (int j = 0; j < NJ; ++j) {
@@ -583,6 +583,61 @@ __global__ __launch_bounds__(256) void split_reduce_kernel(const GemmParams p, c
   if (p.resid_out) st8(p.resid_out + (int64_t)m * p.ldr + n, pack_bf16x4(r[0], r[1], r[2], r[3]));
 }
 
+// The K-parts of a split QKV tile summed in part order, then the QKV epilogue:
+// bias, rotary rotation of Q and K, Q to its buffer and K/V into the pages.
+// One thread per 4 in-head features f..f+3 and their rotary partners
+// f+HD/2..f+HD/2+3 of one token (32 threads per token and tile).
+template <int HD>
+__global__ __launch_bounds__(256) void qkv_split_reduce_kernel(const GemmParams p, const Sched sc) {
+  constexpr int TPH = HD / 8;  // threads per head
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;  // over split tiles x 256 tokens x 32
+  const int ti = (int)(idx / (BM * 32));
+  const int e = (int)(idx % (BM * 32));
+  const int ml = e / 32, c = e % 32;
+  const int n1 = (c / TPH) * HD + 4 * (c % TPH);  // tile column of the first feature
+  int tm, tn;
+  tile_coords(sc.split_first + ti, sc.tiles_m, sc.tiles_n, tm, tn);
+  const int m = tm * BM + ml, r = tn * BN + n1;
+  if (m >= p.M || r >= p.N) return;
+  const float *pp = p.split_part + (int64_t)ti * sc.split_s * BM * BN + ml * BN + n1;
+  f32x4 x1 = *reinterpret_cast<const f32x4 *>(pp), x2 = *reinterpret_cast<const f32x4 *>(pp + HD / 2);
+  for (int sp = 1; sp < sc.split_s; ++sp) {
+    x1 += *reinterpret_cast<const f32x4 *>(pp + (int64_t)sp * BM * BN);
+    x2 += *reinterpret_cast<const f32x4 *>(pp + (int64_t)sp * BM * BN + HD / 2);
+  }
+  int local;
+  const int sg = segment_of<EPI_QKV>(p, r, local);
+  const int head = local / HD, f = local % HD;
+  if (const bf16 *bias = p.bias[sg]) {
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) {
+      x1[jj] += bf2f(bias[head * HD + f + jj]);
+      x2[jj] += bf2f(bias[head * HD + f + HD / 2 + jj]);
+    }
+  }
+  if (sg < 2) {
+    const float2 *cs = p.rope_cs + (int64_t)(p.pos0 + m) * (HD / 2) + f;
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) {
+      const float2 cj = cs[jj];
+      const float y1 = x1[jj] * cj.x - x2[jj] * cj.y;
+      const float y2 = x2[jj] * cj.x + x1[jj] * cj.y;
+      x1[jj] = y1;
+      x2[jj] = y2;
+    }
+  }
+  bf16 *dst;
+  if (sg == 0) {
+    dst = p.q_out + (int64_t)m * p.dq + head * HD;
+  } else {
+    const int64_t prow = paged_row(p.kv, p.pos0 + m, head, HD);
+    if (prow < 0) return;
+    dst = (bf16 *)(sg == 1 ? p.kv.k : p.kv.v) + prow;
+  }
+  st8(dst + f, pack_bf16x4(x1[0], x1[1], x1[2], x1[3]));
+  st8(dst + f + HD / 2, pack_bf16x4(x2[0], x2[1], x2[2], x2[3]));
+}
+
 // U[m, ucol + r] = bf16(scale * sum of the fused down-projection adapter sums
 // of token m): over the runs that cover m's token tile in increasing order of
 // their first tile, then over the two feature halves.  One thread per 4 ranks.
@@ -615,7 +670,7 @@ Sched schedule(GemmEpi epi, const GemmParams &p) {
   const int tiles = sc.tiles_m * sc.tiles_n;
   sc.split_first = tiles;
   sc.split_s = 1;
-  if (epi == EPI_RESID && p.split_part && p.n_cu > 0) {
+  if ((epi == EPI_RESID || epi == EPI_QKV) && p.split_part && p.n_cu > 0) {
     // a last wave at most half full: split its tiles (or all tiles, when there
     // are fewer than compute units) into K-parts of at least 8 slices
     const int r = tiles % p.n_cu;
@@ -676,8 +731,14 @@ hipError_t go(hipStream_t s, const GemmParams &p0, bool *dn_done) {
   if (sc.split_s > 1) {
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    const int64_t n = (int64_t)(sc.tiles_m * sc.tiles_n - sc.split_first) * BM * BN / 4;
-    hipLaunchKernelGGL(split_reduce_kernel, dim3((unsigned)(n / 256)), dim3(256), 0, s, p, sc);
+    const int split_tiles = sc.tiles_m * sc.tiles_n - sc.split_first;
+    if (EPI == EPI_QKV) {
+      const int64_t n = (int64_t)split_tiles * BM * 32;
+      hipLaunchKernelGGL((qkv_split_reduce_kernel<HD>), dim3((unsigned)(n / 256)), dim3(256), 0, s, p, sc);
+    } else {
+      const int64_t n = (int64_t)split_tiles * BM * BN / 4;
+      hipLaunchKernelGGL(split_reduce_kernel, dim3((unsigned)(n / 256)), dim3(256), 0, s, p, sc);
+    }
   }
   return hipGetLastError();
 }
