@@ -126,10 +126,13 @@ int32_t crf_abi_version(void);
  * 0..max_tokens-1.  Besides the per-token buffers (fp32 residual stream,
  * normalised input, queries, attention output, SwiGLU output, LoRA
  * down-projections), a bf16 context holds fixed-size scratch for split
- * work: one 256x256 fp32 tile per compute unit for the residual GEMMs' K-parts
- * (64 MiB on 256 CUs), key-split attention partials for decoding steps
- * (ceil(max_tokens/64) x n_q_heads x 16 x (head_dim+4) floats) and K-split
- * LoRA partials.  All of it is freed by crf_context_destroy.  On success *out
+ * work: one 256x256 fp32 tile per compute unit for the K-parts of the QKV and
+ * residual GEMMs (64 MiB on 256 CUs), key-split attention partials for
+ * decoding steps (ceil(max_tokens/64) x n_q_heads x 16 x (head_dim+4) floats),
+ * K-split LoRA partials and, when max_lora_rank > 0, the down projection's
+ * adapter sums formed inside the gate/up projection (4 x 2 x 256 x 16 floats
+ * per compute unit, 32 MiB on 256 CUs, plus one int per gate/up tile).  All of
+ * it is freed by crf_context_destroy.  On success *out
  * receives the context.  Errors: INVALID_ARG (null), UNSUPPORTED (see
  * crf_validate_dims), HIP (allocation failed). */
 crf_status crf_context_create(const crf_model_dims *dims, int32_t max_tokens, int32_t max_lora_rank,
