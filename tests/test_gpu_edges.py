@@ -98,6 +98,10 @@ def test_prefix_longer_than_workspace_is_rejected():
     # adapters on all seven projections over 8200 tokens: the LoRA down-projections
     # take 64 tokens per workgroup (8 tokens in the last one)
     ("qwen7b_16k", dict(n_layers=4, d_model=256, n_q_heads=2, n_kv_heads=1, head_dim=128, d_ffn=512), 8200),
+    # adapters on all seven projections, 22 token tiles x 16 gate/up tiles on 256
+    # workgroups: 36 workgroups' items cross a token-tile group, so their fused
+    # down-projection adapter sums are flushed as two runs
+    ("qwen7b_16k", dict(n_layers=4, d_model=768, n_q_heads=12, n_kv_heads=2, head_dim=64, d_ffn=2048), 5500),
 ])
 def test_bf16_longer_prefixes(base, dims, n):
     """Longer ragged prefixes (dozens of query blocks per head, more query
