@@ -53,6 +53,7 @@ constexpr int DN_RANK = 16;
 constexpr int DN_BYTES = 2 * BM * DN_RANK * 4;
 static_assert(BK == 32 || BK == 64, "slice width");
 static_assert(STAGES >= 2 && STAGE_BYTES <= 160 * 1024, "LDS budget");
+static_assert(BM * BK * 2 / 1024 >= 2 * WAVES, "each wave owns two x blocks of a stage");
 
 // Chunk c of slice row r sits at position c ^ s(r), s(r) = (r / 2) % 8 for
 // 128-byte rows and (r / 4) % 4 for 64-byte rows: the 16 rows one quarter of a
@@ -248,6 +249,25 @@ __global__ __launch_bounds__(64 * WAVES, 1) void gemm_bf16_kernel(const GemmPara
     }
   };
   if (dn_on) dn_zero();
+  // The factor rows A_down[0..16)[fb, fb + 64) of this wave's 64 features go,
+  // right after the last slice's barrier, into x blocks `wave` and
+  // `WAVES + wave` of the stage that slice used: nobody reads that stage
+  // again, and only this wave refills those blocks (after the epilogue).
+  // Instruction t, lane L: rank 8 t + L / 8, features fb + 8 (L % 8) ..+8
+  // (ranks at or past dn_rank read as zero).
+  int dn_fb = 0;
+  auto dn_fetch = [&](int stage) {
+    lds_char *dx = (lds_char *)(lds_x + stage * BM * BK);
+    const __amdgpu_buffer_rsrc_t dres = make_rsrc(p.dn_a, (uint32_t)((int64_t)p.dn_rank * p.d_ffn * 2));
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      const int r = 8 * t + lane / 8;
+      const uint32_t vo = r < p.dn_rank && dn_fb < p.d_ffn
+                              ? (uint32_t)(((int64_t)r * p.d_ffn + dn_fb + 8 * (lane % 8)) * 2)
+                              : CRF_OOB;
+      dma16(dres, dx + (t * WAVES + wave) * 1024, vo, 0);
+    }
+  };
 
   f32x16 acc[4][NJ];
 #pragma unroll
@@ -317,6 +337,8 @@ __global__ __launch_bounds__(64 * WAVES, 1) void gemm_bf16_kernel(const GemmPara
     if constexpr (!LAST) {
       produce(st);
       frag(nst, 0, a0, b0);
+    } else {
+      if (dn_on) dn_fetch(st);
     }
     mm(a1, b1);  // KSTEPS is even: the last k-step of a slice uses (a1, b1)
     interleave(std::integral_constant<int, LAST ? 0 : DMA_PER_SLICE>());
@@ -346,6 +368,7 @@ __global__ __launch_bounds__(64 * WAVES, 1) void gemm_bf16_kernel(const GemmPara
     const int part = it.part;
 
     for (int kt = it.kb; kt + 1 < it.ke; ++kt) slice(std::false_type());
+    if (EPI == EPI_SWIGLU) dn_fb = (n0 + wn * 128) / 2;
     slice(std::true_type());
 
     // ---- low-rank delta: acc += U[token, ucol_s + k] * lb_s[feature, k] (K-part 0 only)
@@ -443,6 +466,20 @@ __global__ __launch_bounds__(64 * WAVES, 1) void gemm_bf16_kernel(const GemmPara
               o[jj] = gt * __builtin_amdgcn_rcpf(1.0f + __expf(-gt)) * up;
             }
             packed[ii][q] = pack_bf16x4(o[0], o[1], o[2], o[3]);
+          }
+        // the factor rows' DMA is the only memory operation in flight here
+        // (the deferred refill comes after the epilogue): wait for it after
+        // the first block's activations (the operands pin the wait there) and
+        // before the first act store, so the wait covers nothing else
+        if (dn_on && j == 0)
+          asm volatile("s_waitcnt vmcnt(0)" ::"v"(packed[0][0]), "v"(packed[0][1]), "v"(packed[0][2]),
+                       "v"(packed[0][3]), "v"(packed[1][0]), "v"(packed[1][1]), "v"(packed[1][2]),
+                       "v"(packed[1][3])
+                       : "memory");
+#pragma unroll
+        for (int ii = 0; ii < 2; ++ii)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
             const int f = fbase + 32 * ii + 8 * q + 4 * g;
             if (m < p.M && f < p.d_ffn) st8(p.act + (int64_t)m * p.d_ffn + f, packed[ii][q]);
           }
@@ -459,13 +496,13 @@ __global__ __launch_bounds__(64 * WAVES, 1) void gemm_bf16_kernel(const GemmPara
           for (int ii = 0; ii < 2; ++ii)
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
-              const int f0 = fbase + 32 * ii + 16 * h + 4 * g;
-              u32x4 av = {0u, 0u, 0u, 0u};
-              if (l32 < p.dn_rank) {
-                const bf16 *ar = p.dn_a + (int64_t)l32 * p.d_ffn + f0;
-                const u32x2 lo = ld8(ar), hi = ld8(ar + 8);
-                av = u32x4{lo[0], lo[1], hi[0], hi[1]};
-              }
+              // features fbase + 32 ii + 16 h + 4 g ..+4 and 8 further, from
+              // 8-feature groups 4 ii + 2 h and 4 ii + 2 h + 1 of row l32
+              const int r = l32 & 15;
+              const char *ar = (const char *)(lds_x + st * BM * BK) + ((r >> 3) * WAVES + wave) * 1024 +
+                               (r & 7) * 128 + (4 * ii + 2 * h) * 16 + 8 * g;
+              const u32x2 lo = *reinterpret_cast<const u32x2 *>(ar), hi = *reinterpret_cast<const u32x2 *>(ar + 16);
+              const u32x4 av = l32 < DN_RANK ? u32x4{lo[0], lo[1], hi[0], hi[1]} : u32x4{0u, 0u, 0u, 0u};
               const u32x4 bv = {packed[ii][2 * h][0], packed[ii][2 * h][1], packed[ii][2 * h + 1][0],
                                 packed[ii][2 * h + 1][1]};
               ud = mfma32(as_bf16x8(av), as_bf16x8(bv), ud);
