@@ -24,6 +24,37 @@ import sys
 import time
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
+CSRC = os.path.join(ROOT, "paper_2609_30884_amd", "csrc")
+# the sources each kernel family is built from: a stored HBM-traffic figure
+# counts only while they are byte for byte the ones the counters ran on
+TRAFFIC_SOURCES = {"gemm": ("gemm_bf16.hip", "common.hpp", "kernels.hpp"),
+                   "attn": ("attn_bf16.hip", "common.hpp", "kernels.hpp")}
+
+
+def kernel_sources_digest(kernel: str) -> str | None:
+    files = TRAFFIC_SOURCES.get(kernel.split("_")[0])
+    if not files:
+        return None
+    import hashlib
+    h = hashlib.sha256()
+    for f in files:
+        with open(os.path.join(CSRC, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def stored_traffic(kernel: str, workload: str):
+    """HBM bytes per launch from profiles/traffic_<kernel>_<workload>.json
+    (copy-calibrated FETCH_SIZE + WRITE_SIZE), or None when there is none or
+    the kernel's sources have changed since the counters were taken."""
+    prof = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload}.json")
+    try:
+        rec = json.load(open(prof))
+    except (OSError, ValueError):
+        return None
+    if rec.get("sources_sha256") != kernel_sources_digest(kernel):
+        return None
+    return rec.get("bytes_per_launch")
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
@@ -220,13 +251,7 @@ def main():
     dom_avg_s = timing[dom][0] / timing[dom][1] * 1e-3
     achieved = kflops[dom] / dom_avg_s
     peak = PEAK_BF16 if dims.dtype == "bf16" else PEAK_F32_VALU
-    traffic = None
-    prof = os.path.join(ROOT, "profiles", f"traffic_{dom}_{wl.name}.json")
-    if os.path.exists(prof):
-        try:
-            traffic = json.load(open(prof)).get("bytes_per_launch")
-        except Exception:
-            traffic = None
+    traffic = stored_traffic(dom, wl.name)
 
     out = {
         "metric": METRIC,

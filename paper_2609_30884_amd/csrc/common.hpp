@@ -53,9 +53,6 @@ CRF_DEV __amdgpu_buffer_rsrc_t make_rsrc(const void *base, uint32_t bytes) {
 CRF_DEV u32x4 bld16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
   return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
 }
-CRF_DEV u32x2 bld8(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
-  return __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, 0));
-}
 constexpr uint32_t CRF_OOB = 0x80000000u;  // any offset >= this is outside every resource we build
 
 // 16-byte-per-lane DMA from a buffer resource straight into LDS: lane L's bytes
