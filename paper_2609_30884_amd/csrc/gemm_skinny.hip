@@ -39,7 +39,10 @@ CRF_DEV const bf16 *skinny_weight_row(const GemmParams &p, GemmEpi epi, int r, i
 template <int EPI, int NB, int W>
 __global__ __launch_bounds__(64 * W) void gemm_skinny_kernel(const GemmParams p) {
   __shared__ f32x4 red[W][NB][64];
-  const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
+  // wave-uniform in a scalar register, so that the k-step guards are scalar
+  // branches: an MFMA in an EXEC-masked block still updates its accumulators
+  // when the mask is empty
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / 64), lane = threadIdx.x % 64;
   const int f0 = blockIdx.x * 16;  // first output feature of the workgroup
   const int nrows = EPI == EPI_SWIGLU ? p.d_ffn : p.N;
   const int tok = min(lane % 16, p.M - 1);  // rows past M repeat the last token; never stored

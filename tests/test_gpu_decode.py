@@ -56,6 +56,10 @@ SPLIT_CASES = {
     # 16 rows x 12 heads do not fit one tile: one workgroup per query head
     "per_head_hd128": ("qwen15b_4k", dict(n_layers=2, d_model=1536, n_q_heads=12, n_kv_heads=1, head_dim=128,
                                           d_ffn=2048), 600, 16, 1024),
+    # d_ffn = 33 x 64: the down projection's 66 k-steps leave a partial last
+    # batch of k-steps in the projection and LoRA kernels
+    "ragged_ffn": ("qwen7b_16k", dict(n_layers=2, d_model=768, n_q_heads=12, n_kv_heads=2, head_dim=64,
+                                      d_ffn=2112), 500, 4, 1024),
 }
 
 

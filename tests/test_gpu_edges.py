@@ -114,3 +114,22 @@ def test_bf16_longer_prefixes(base, dims, n):
     torch.cuda.synchronize()
     out, kv = oracle_window(case)
     assert_window_parity(case, out, kv, label=f"longer prefix n={n}")
+
+
+@pytest.mark.parametrize("rank,d_ffn", [(8, 2112), (16, 2112), (32, 2112)])
+def test_bf16_adapter_ranks(rank, d_ffn):
+    """Adapters on all seven projections at ranks below, at and above the
+    16 that the gate/up epilogue's fused down-projection sums take (rank 32
+    goes through the separate down-projection pass), with d_ffn = 33 x 64, so
+    the last gate/up tile holds only gate/up rows of 64 features and its
+    second feature half lies past d_ffn."""
+    from synthetic.device import build_case
+    base = syn.WORKLOADS["qwen7b_16k"].with_dims(n_layers=4, d_model=768, n_q_heads=12, n_kv_heads=2, head_dim=64,
+                                                  d_ffn=d_ffn)
+    wl = dataclasses.replace(base.with_window(n_tokens=700, l0=1, h=2), lora_rank=rank)
+    print(f"[case] adapter rank {rank} d_ffn {d_ffn} n=700", flush=True)
+    case = build_case(wl, 31)
+    run_gpu_window(case)
+    torch.cuda.synchronize()
+    out, kv = oracle_window(case)
+    assert_window_parity(case, out, kv, label=f"rank {rank} d_ffn {d_ffn}")
