@@ -107,3 +107,23 @@ def test_context_requires_device_or_reports_hip_error():
     with pytest.raises(crf.CrfError) as ei:
         crf.Context(dims(), 16, 16)
     assert ei.value.status == 6
+
+
+def test_mfma_kernels_keep_wave_index_scalar():
+    """Kernels that issue MFMAs take their wave index through readfirstlane.
+    A wave index derived per lane makes wave-uniform guards EXEC-masked
+    blocks, and an MFMA in such a block still updates its accumulators when
+    the mask is empty (this once added a stale k-step to the LoRA
+    down-projection)."""
+    import glob
+    import re
+    csrc = os.path.join(ROOT, "paper_2609_30884_amd", "csrc")
+    checked = 0
+    for path in sorted(glob.glob(os.path.join(csrc, "*.hip"))):
+        src = open(path).read()
+        if "mfma" not in src:
+            continue
+        for m in re.finditer(r"\bconst int wave\s*=\s*([^;,]+)", src):
+            assert "readfirstlane" in m.group(1), f"{os.path.basename(path)}: wave = {m.group(1)}"
+            checked += 1
+    assert checked >= 4
