@@ -45,13 +45,18 @@ __global__ __launch_bounds__(64 * NW) void lora_down_kernel(LdArgs a) {
   const bf16 *xrow[TB];
 #pragma unroll
   for (int tb = 0; tb < TB; ++tb) xrow[tb] = a.X + (int64_t)min(m0 + 16 * tb + lane % 16, a.M - 1) * a.ldx + kq;
-  // per block: factor row pointer (or null -> zeros)
-  const bf16 *arow[NB];
+  // per block: the target's factor as a buffer resource and this lane's row
+  // offset; rows past the rank (and absent targets) lie out of range and read
+  // as zero, so the loads need no branch
+  __amdgpu_buffer_rsrc_t ares[NB];
+  uint32_t aoff[NB];
 #pragma unroll
   for (int b = 0; b < NB; ++b) {
     const int t = (b * 16) / a.rank_pad;
     const int j = b * 16 - t * a.rank_pad + lane % 16;
-    arow[b] = (a.A[t] && j < a.rank[t]) ? a.A[t] + (int64_t)j * a.K + kq : nullptr;
+    const bool on = a.A[t] != nullptr;
+    ares[b] = make_rsrc(on ? (const void *)a.A[t] : (const void *)a.X, on ? (uint32_t)(a.rank[t] * a.K * 2) : 0u);
+    aoff[b] = on && j < a.rank[t] ? (uint32_t)((j * a.K + kq) * 2) : CRF_OOB;
   }
   f32x4 acc[NB][TB];
 #pragma unroll
@@ -69,7 +74,7 @@ __global__ __launch_bounds__(64 * NW) void lora_down_kernel(LdArgs a) {
         for (int tb = 0; tb < TB; ++tb) xb[u][tb] = as_bf16x8(ld16(xrow[tb] + k));
 #pragma unroll
         for (int b = 0; b < NB; ++b)
-          ab[u][b] = arow[b] ? as_bf16x8(ld16(arow[b] + k)) : as_bf16x8(u32x4{0u, 0u, 0u, 0u});
+          ab[u][b] = as_bf16x8(bld16(ares[b], aoff[b], (uint32_t)k * 2));
       }
     }
     __builtin_amdgcn_sched_barrier(0);  // every load of the batch in flight before the first MFMA
