@@ -133,3 +133,33 @@ def test_bf16_adapter_ranks(rank, d_ffn):
     torch.cuda.synchronize()
     out, kv = oracle_window(case)
     assert_window_parity(case, out, kv, label=f"rank {rank} d_ffn {d_ffn}")
+
+
+@pytest.mark.parametrize("kind,h", [("small", 1), ("small", 2), ("f32", 2)])
+def test_hidden_out_may_alias_the_boundary_state(kind, h):
+    """hidden_out on the same buffer as hidden_at_boundary gives bitwise the
+    output and pages of a run into a separate buffer."""
+    import paper_2609_30884_amd as crf
+    from synthetic.device import build_case, canary_fill
+    if kind == "f32":
+        wl = syn.WORKLOADS["tiny_f32"].with_window(n_tokens=150, l0=1, h=h)
+    else:
+        wl = _wl("small", 300)
+        wl = wl.with_window(l0=1, h=h)
+    print(f"[case] aliasing {kind} h={h}", flush=True)
+    case = build_case(wl, 5)
+    run_gpu_window(case)
+    torch.cuda.synchronize()
+    out_sep = case.hidden_out.clone()
+    k_sep, v_sep = case.k_pool.clone(), case.v_pool.clone()
+    canary_fill(case.k_pool)
+    canary_fill(case.v_pool)
+    buf = case.hidden_dev.clone()
+    cd = cdims(wl.dims)
+    ctx = crf.Context(cd, wl.windows[0].n_tokens, wl.lora_rank)
+    kv = crf.kv_cache(case.k_pool, case.v_pool, case.block_table_dev, wl.windows[0].n_tokens, wl.page_size)
+    crf.recompute_window(ctx, cd, buf, crf.layer_weights_array(case.weights_dev),
+                         crf.lora_array(case.lora_dev, wl.dims.n_layers), 1, h, kv, buf)
+    torch.cuda.synchronize()
+    assert bits_equal(buf, out_sep)
+    assert bits_equal(case.k_pool, k_sep) and bits_equal(case.v_pool, v_sep)
