@@ -260,6 +260,12 @@ crf_status crf_context_device_errors(crf_context *ctx, int32_t *flags_out);
  * synchronises those events and returns, per kernel class (CRF_KK_*), the
  * summed milliseconds and launch counts since the last read, then resets. */
 crf_status crf_context_set_timing(crf_context *ctx, int32_t enable);
+/* The same for a subset of kernel classes: bit k of class_mask enables class
+ * k (CRF_KK_*), 0 disables timing; enable != 0 above is the mask of every
+ * class.  Each bracketed launch costs two event records on its stream, so a
+ * measurement that needs one class's launch times only brackets that class.
+ * Errors: INVALID_ARG (null context, bits at or past CRF_KK_COUNT). */
+crf_status crf_context_set_timing_classes(crf_context *ctx, uint32_t class_mask);
 crf_status crf_context_read_timing(crf_context *ctx, float *ms_out, int32_t *count_out, int32_t n_kinds);
 
 /* Device facts for reporting measurements against the hardware's peak:

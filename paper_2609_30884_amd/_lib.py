@@ -68,7 +68,8 @@ _LIB: Optional[ctypes.CDLL] = None
 
 EXPORTS = ("crf_status_string", "crf_abi_version", "crf_context_create", "crf_context_destroy", "crf_last_error",
            "crf_validate_dims", "crf_validate_window", "crf_recompute_window", "crf_recompute_window_batched",
-           "crf_layer_drift", "crf_context_device_errors", "crf_context_set_timing", "crf_context_read_timing",
+           "crf_layer_drift", "crf_context_device_errors", "crf_context_set_timing", "crf_context_set_timing_classes",
+           "crf_context_read_timing",
            "crf_device_info", "crf_decode_logits")
 
 
@@ -106,6 +107,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.crf_context_device_errors.argtypes = [VP, P(I32)]
     lib.crf_context_set_timing.restype = I32
     lib.crf_context_set_timing.argtypes = [VP, I32]
+    lib.crf_context_set_timing_classes.restype = I32
+    lib.crf_context_set_timing_classes.argtypes = [VP, ctypes.c_uint32]
     lib.crf_context_read_timing.restype = I32
     lib.crf_context_read_timing.argtypes = [VP, P(ctypes.c_float), P(I32), I32]
     lib.crf_decode_logits.restype = I32
@@ -219,8 +222,16 @@ class Context:
         _err(self.lib, self.handle, self.lib.crf_context_device_errors(self.handle, ctypes.byref(out)))
         return int(out.value)
 
-    def set_timing(self, on: bool):
-        _err(self.lib, self.handle, self.lib.crf_context_set_timing(self.handle, 1 if on else 0))
+    def set_timing(self, on: bool, classes=None):
+        """Event timing of every kernel class (on), of none, or of the named
+        classes only (KERNEL_KINDS names)."""
+        if classes is None:
+            _err(self.lib, self.handle, self.lib.crf_context_set_timing(self.handle, 1 if on else 0))
+            return
+        mask = 0
+        for name in classes if on else ():
+            mask |= 1 << KERNEL_KINDS.index(name)
+        _err(self.lib, self.handle, self.lib.crf_context_set_timing_classes(self.handle, mask))
 
     def read_timing(self) -> Dict[str, Tuple[float, int]]:
         n = len(KERNEL_KINDS)

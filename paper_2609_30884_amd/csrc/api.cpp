@@ -19,7 +19,7 @@ namespace {
 thread_local std::string g_last_error;
 
 struct Timer {
-  bool on = false;
+  uint32_t mask = 0;            // bit k: launches of class k are bracketed by events
   std::vector<hipEvent_t> ev;   // pairs (start, stop)
   std::vector<int> kind;        // per pair
   size_t used = 0;              // pairs recorded since last read
@@ -206,9 +206,10 @@ struct Launch {
   hipStream_t s;
   int kind;
   size_t idx = 0;
-  Launch(crf_context *c, hipStream_t st, int k) : ctx(c), s(st), kind(k) {
+  bool on;
+  Launch(crf_context *c, hipStream_t st, int k) : ctx(c), s(st), kind(k), on(((c->timer.mask >> k) & 1u) != 0) {
     Timer &t = ctx->timer;
-    if (!t.on) return;
+    if (!on) return;
     idx = t.used;
     if (2 * idx + 2 > t.ev.size()) {
       hipEvent_t a, b;
@@ -222,7 +223,7 @@ struct Launch {
   }
   ~Launch() {
     Timer &t = ctx->timer;
-    if (!t.on || 2 * idx + 2 > t.ev.size()) return;
+    if (!on || 2 * idx + 2 > t.ev.size()) return;
     (void)hipEventRecord(t.ev[2 * idx + 1], s);
     t.used = idx + 1;
   }
@@ -798,8 +799,13 @@ crf_status crf_context_device_errors(crf_context *ctx, int32_t *flags_out) {
 }
 
 crf_status crf_context_set_timing(crf_context *ctx, int32_t enable) {
+  return crf_context_set_timing_classes(ctx, enable ? (1u << CRF_KK_COUNT) - 1u : 0u);
+}
+
+crf_status crf_context_set_timing_classes(crf_context *ctx, uint32_t class_mask) {
   if (!ctx) return fail(nullptr, CRF_ERR_INVALID_ARG, "context is NULL");
-  ctx->timer.on = enable != 0;
+  if (class_mask >> CRF_KK_COUNT) return fail(ctx, CRF_ERR_INVALID_ARG, "class mask 0x%x has bits past CRF_KK_COUNT", class_mask);
+  ctx->timer.mask = class_mask;
   return CRF_OK;
 }
 

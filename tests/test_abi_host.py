@@ -127,3 +127,9 @@ def test_mfma_kernels_keep_wave_index_scalar():
             assert "readfirstlane" in m.group(1), f"{os.path.basename(path)}: wave = {m.group(1)}"
             checked += 1
     assert checked >= 4
+
+
+def test_timing_classes_rejects_null_context():
+    lib = crf.load()
+    assert lib.crf_context_set_timing_classes(None, 1) == 1  # CRF_ERR_INVALID_ARG
+    assert lib.crf_context_set_timing(None, 1) == 1
