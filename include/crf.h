@@ -203,8 +203,17 @@ typedef struct {
 /* crf_recompute_window over several independent stale caches of one base
  * model, each with its own boundary state, window and adapter version (the
  * per-cache decision of Sec. 4.1 applied to many caches at once).  Every item
- * is validated before anything is launched; items run in order on `stream`.
- * Errors: as crf_recompute_window; the failing item's index is in the message. */
+ * is validated before anything is launched.  When the items are independent
+ * (pairwise distinct k_pool and v_pool, and no item's hidden_out is another
+ * item's hidden_out or hidden_at_boundary) and event timing is off, they run
+ * on two internal streams that wait for `stream` and that `stream` then waits
+ * for, longest windows first, each on the lane with less work so far; the
+ * first such call allocates a second workspace as large as the context's own
+ * (what crf_context_create allocates) and two streams, kept until
+ * crf_context_destroy.  Otherwise items run in order on `stream`.  Results are
+ * the same either way (each item's arithmetic does not depend on the lane).
+ * Errors: as crf_recompute_window; the failing item's index is in the message;
+ * WORKSPACE if the second workspace cannot be allocated. */
 crf_status crf_recompute_window_batched(crf_context *ctx, const crf_model_dims *dims,
                                         const crf_layer_weights *base_weights, int32_t n_items,
                                         const crf_window_item *items, void *stream);

@@ -66,6 +66,12 @@ struct crf_context {
   bool drift_ev_recorded = false;
   std::string last_error;
   Timer timer;
+  // batched calls over independent caches: a second workspace (a context of
+  // the same shape, made by the first such call) and two lane streams forked
+  // from the caller's stream
+  crf_context *lane2 = nullptr;
+  hipStream_t lane_s[2] = {nullptr, nullptr};
+  hipEvent_t fork_ev = nullptr, join_ev[2] = {nullptr, nullptr};
 };
 
 namespace {
@@ -546,6 +552,12 @@ void crf_context_destroy(crf_context *ctx) {
   if (ctx->drift_host) (void)hipHostFree(ctx->drift_host);
   if (ctx->drift_ev) (void)hipEventDestroy(ctx->drift_ev);
   for (hipEvent_t e : ctx->timer.ev) (void)hipEventDestroy(e);
+  for (int i = 0; i < 2; ++i) {
+    if (ctx->lane_s[i]) (void)hipStreamDestroy(ctx->lane_s[i]);
+    if (ctx->join_ev[i]) (void)hipEventDestroy(ctx->join_ev[i]);
+  }
+  if (ctx->fork_ev) (void)hipEventDestroy(ctx->fork_ev);
+  crf_context_destroy(ctx->lane2);
   delete ctx;
 }
 
@@ -641,13 +653,68 @@ crf_status crf_recompute_window_batched(crf_context *ctx, const crf_model_dims *
                                   it.hidden_out, what);
     if (st != CRF_OK) return st;
   }
-  for (int i = 0; i < n_items; ++i) {
-    const crf_window_item &it = items[i];
-    crf_status st = run_window(ctx, it.hidden_at_boundary, base_weights, it.lora, it.l0, it.h, &it.kv, it.hidden_out,
-                               (hipStream_t)stream);
-    if (st != CRF_OK) return st;
+  // Independent items (no item writes a buffer that another reads or writes)
+  // run on two lanes, each a stream with its own workspace, so that small
+  // windows fill the GPU together; every item's arithmetic is the same either
+  // way.  While event timing is on they run in order on `stream`.
+  bool lanes = n_items >= 2 && ctx->timer.mask == 0;
+  for (int i = 0; lanes && i < n_items; ++i)
+    for (int j = 0; lanes && j < n_items; ++j) {
+      if (i == j) continue;
+      const crf_window_item &a = items[i], &b = items[j];
+      if (a.kv.k_pool == b.kv.k_pool || a.kv.v_pool == b.kv.v_pool || a.kv.k_pool == b.kv.v_pool)
+        lanes = false;
+      if (a.hidden_out && (a.hidden_out == b.hidden_out || a.hidden_out == b.hidden_at_boundary)) lanes = false;
+    }
+  if (!lanes) {
+    for (int i = 0; i < n_items; ++i) {
+      const crf_window_item &it = items[i];
+      crf_status st = run_window(ctx, it.hidden_at_boundary, base_weights, it.lora, it.l0, it.h, &it.kv,
+                                 it.hidden_out, (hipStream_t)stream);
+      if (st != CRF_OK) return st;
+    }
+    return CRF_OK;
   }
-  return CRF_OK;
+  if (!ctx->fork_ev) {  // set last: it marks the lanes complete
+    if (!ctx->lane2) {
+      crf_context *c2 = nullptr;
+      if (crf_context_create(&ctx->dims, ctx->max_tokens, ctx->max_rank, &c2) != CRF_OK)
+        return fail(ctx, CRF_ERR_WORKSPACE, "second workspace for concurrent batch items: %s", g_last_error.c_str());
+      ctx->lane2 = c2;
+    }
+    for (int i = 0; i < 2; ++i) {
+      if (!ctx->lane_s[i]) HIP_TRY(ctx, hipStreamCreateWithFlags(&ctx->lane_s[i], hipStreamNonBlocking));
+      if (!ctx->join_ev[i]) HIP_TRY(ctx, hipEventCreateWithFlags(&ctx->join_ev[i], hipEventDisableTiming));
+    }
+    HIP_TRY(ctx, hipEventCreateWithFlags(&ctx->fork_ev, hipEventDisableTiming));
+  }
+  // longest first, each to the lane with less work so far
+  std::vector<int> order(n_items);
+  for (int i = 0; i < n_items; ++i) order[i] = i;
+  auto work = [&](int i) { return (int64_t)items[i].kv.n_tokens * items[i].h; };
+  std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return work(a) > work(b); });
+  HIP_TRY(ctx, hipEventRecord(ctx->fork_ev, (hipStream_t)stream));
+  for (int i = 0; i < 2; ++i) HIP_TRY(ctx, hipStreamWaitEvent(ctx->lane_s[i], ctx->fork_ev, 0));
+  int64_t load[2] = {0, 0};
+  crf_status st = CRF_OK;
+  for (int i : order) {
+    const int lane = load[1] < load[0] ? 1 : 0;
+    load[lane] += work(i);
+    crf_context *c = lane ? ctx->lane2 : ctx;
+    const crf_window_item &it = items[i];
+    st = run_window(c, it.hidden_at_boundary, base_weights, it.lora, it.l0, it.h, &it.kv, it.hidden_out,
+                    ctx->lane_s[lane]);
+    if (st != CRF_OK) {
+      if (c != ctx) ctx->last_error = c->last_error;
+      break;
+    }
+  }
+  // join both lanes back into the caller's stream, also after a failed launch
+  for (int i = 0; i < 2; ++i) {
+    HIP_TRY(ctx, hipEventRecord(ctx->join_ev[i], ctx->lane_s[i]));
+    HIP_TRY(ctx, hipStreamWaitEvent((hipStream_t)stream, ctx->join_ev[i], 0));
+  }
+  return st;
 }
 
 crf_status crf_decode_logits(crf_context *ctx, const crf_model_dims *dims, const void *new_tokens, int32_t n_new,
@@ -794,6 +861,12 @@ crf_status crf_context_device_errors(crf_context *ctx, int32_t *flags_out) {
   int v = 0;
   HIP_TRY(ctx, hipMemcpy(&v, ctx->d_err, sizeof(int), hipMemcpyDeviceToHost));
   HIP_TRY(ctx, hipMemset(ctx->d_err, 0, sizeof(int)));
+  if (ctx->lane2) {  // the second workspace's flags (concurrent batch items)
+    int v2 = 0;
+    HIP_TRY(ctx, hipMemcpy(&v2, ctx->lane2->d_err, sizeof(int), hipMemcpyDeviceToHost));
+    HIP_TRY(ctx, hipMemset(ctx->lane2->d_err, 0, sizeof(int)));
+    v |= v2;
+  }
   *flags_out = v;
   return CRF_OK;
 }

@@ -287,3 +287,75 @@ def test_batched_validates_every_item_first():
     torch.cuda.synchronize()
     from synthetic.device import canary_mask
     assert bool(canary_mask(c.k_pool).all()), "nothing may run when any item is invalid"
+
+
+def _batched_cases(windows, seed=7):
+    from synthetic.device import build_case
+    base = syn.WORKLOADS["qwen15b_mixed8"]
+    layers = sorted({l for w in windows for l in range(w.l0, w.l0 + w.h)})
+    cases = [build_case(base, seed, window=w, item=i, layers=layers) for i, w in enumerate(windows)]
+    for c in cases[1:]:
+        c.weights_dev = cases[0].weights_dev
+        c.weights = cases[0].weights
+    return base, cases
+
+
+def test_batched_lanes_match_in_order_run():
+    """Independent items run on two lanes with timing off and in order with
+    timing on: outputs and pages bitwise the same."""
+    import paper_2609_30884_amd as crf
+    from synthetic.device import canary_fill
+    base, cases = _batched_cases([syn.Window(700, 3, 2), syn.Window(257, 26, 2), syn.Window(1030, 10, 1),
+                                  syn.Window(64, 0, 3), syn.Window(1, 5, 1)])
+    cd = cdims(base.dims)
+    ctx = crf.Context(cd, max(c.window.n_tokens for c in cases), base.lora_rank)
+    keep, its = [], []
+    for c in cases:
+        la = crf.lora_array(c.lora_dev, base.dims.n_layers)
+        keep.append(la)
+        kv = crf.kv_cache(c.k_pool, c.v_pool, c.block_table_dev, c.window.n_tokens, base.page_size)
+        its.append(crf.window_item(c.hidden_dev, la, c.window.l0, c.window.h, kv, c.hidden_out))
+    w = crf.layer_weights_array(cases[0].weights_dev)
+    print("[case] batched lanes vs in-order", flush=True)
+    ctx.set_timing(True)
+    crf.recompute_window_batched(ctx, cd, w, its)
+    torch.cuda.synchronize()
+    ctx.set_timing(False)
+    ctx.read_timing()
+    ref = [(c.hidden_out.clone(), c.k_pool.clone(), c.v_pool.clone()) for c in cases]
+    for c in cases:
+        canary_fill(c.k_pool)
+        canary_fill(c.v_pool)
+        c.hidden_out.zero_()
+    for _ in range(2):  # the second call reuses the lanes made by the first
+        crf.recompute_window_batched(ctx, cd, w, its)
+    torch.cuda.synchronize()
+    assert ctx.device_errors() == 0
+    for c, (h, k, v) in zip(cases, ref):
+        assert bits_equal(c.hidden_out, h) and bits_equal(c.k_pool, k) and bits_equal(c.v_pool, v)
+
+
+def test_batched_chained_items_run_in_order():
+    """An item whose boundary state is another item's output is not
+    independent: the batch runs in order and the second item sees the first
+    one's output."""
+    import paper_2609_30884_amd as crf
+    base, cases = _batched_cases([syn.Window(300, 2, 1), syn.Window(300, 3, 1)])
+    cd = cdims(base.dims)
+    ctx = crf.Context(cd, 300, base.lora_rank)
+    las = [crf.lora_array(c.lora_dev, base.dims.n_layers) for c in cases]
+    kvs = [crf.kv_cache(c.k_pool, c.v_pool, c.block_table_dev, 300, base.page_size) for c in cases]
+    mid = torch.empty_like(cases[0].hidden_out)
+    its = [crf.window_item(cases[0].hidden_dev, las[0], 2, 1, kvs[0], mid),
+           crf.window_item(mid, las[1], 3, 1, kvs[1], cases[1].hidden_out)]
+    w = crf.layer_weights_array(cases[0].weights_dev)
+    print("[case] batched chained items", flush=True)
+    crf.recompute_window_batched(ctx, cd, w, its)
+    torch.cuda.synchronize()
+    got = cases[1].hidden_out.clone()
+    # the same two windows as separate calls, in order
+    mid2 = torch.empty_like(mid)
+    crf.recompute_window(ctx, cd, cases[0].hidden_dev, w, las[0], 2, 1, kvs[0], mid2)
+    crf.recompute_window(ctx, cd, mid2, w, las[1], 3, 1, kvs[1], cases[1].hidden_out)
+    torch.cuda.synchronize()
+    assert bits_equal(mid, mid2) and bits_equal(got, cases[1].hidden_out)
