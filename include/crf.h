@@ -145,8 +145,9 @@ const char *crf_last_error(const crf_context *ctx);
 
 /* Host-only check of a decoder shape: every dimension positive,
  * n_q_heads % n_kv_heads == 0, head_dim in {64, 128}, and for bf16 the
- * projection widths multiples of 128 and d_ffn a multiple of 64.  Touches no
- * device.  Errors: INVALID_ARG, SHAPE, UNSUPPORTED. */
+ * projection widths multiples of 128, d_ffn a multiple of 64 and every
+ * projection weight matrix smaller than 2 GiB.  Touches no device.
+ * Errors: INVALID_ARG, SHAPE, UNSUPPORTED. */
 crf_status crf_validate_dims(const crf_model_dims *dims);
 
 /* Host-only check of a recomputation request (Sec. 4.1: the candidate window
@@ -156,7 +157,10 @@ crf_status crf_validate_dims(const crf_model_dims *dims);
  * n_tokens >= 0, n_tokens <= n_pages * page_size, page_stride >=
  * n_kv_heads*page_size*head_dim, layer_stride >= n_pages*page_stride (else
  * SHAPE), one layer of a pool (n_pages*page_stride elements) under 2 GiB
- * (else UNSUPPORTED), non-null pools and block table when h > 0 and
+ * (else UNSUPPORTED), on the bf16 path with h > 0 and more than 16 tokens a
+ * projection input of n_tokens x max(d_model, n_q_heads*head_dim, d_ffn)
+ * elements under 2 GiB (else UNSUPPORTED: 56,679 tokens at most at
+ * Qwen2.5-7B shapes), non-null pools and block table when h > 0 and
  * n_tokens > 0 (else INVALID_ARG).  Touches no device. */
 crf_status crf_validate_window(const crf_model_dims *dims, int32_t l0, int32_t h, const crf_kv_cache *kv);
 
@@ -204,14 +208,19 @@ typedef struct {
  * model, each with its own boundary state, window and adapter version (the
  * per-cache decision of Sec. 4.1 applied to many caches at once).  Every item
  * is validated before anything is launched.  When the items are independent
- * (pairwise distinct k_pool and v_pool, and no item's hidden_out is another
- * item's hidden_out or hidden_at_boundary) and event timing is off, they run
+ * and event timing is off, they run
  * on two internal streams that wait for `stream` and that `stream` then waits
  * for, longest windows first, each on the lane with less work so far; the
  * first such call allocates a second workspace as large as the context's own
  * (what crf_context_create allocates) and two streams, kept until
- * crf_context_destroy.  Otherwise items run in order on `stream`.  Results are
- * the same either way (each item's arithmetic does not depend on the lane).
+ * crf_context_destroy.  Otherwise items run in order on `stream`.  Items are
+ * independent when no byte one item may write lies in a range another item
+ * may read or write: an item writes the layers [l0, l0+h) of both pools (each
+ * layer's whole n_pages*page_stride span, since the pages are chosen by the
+ * device-side block table) and its hidden_out, and reads those pool spans,
+ * its hidden_at_boundary and its block table.  Items with h == 0 or no tokens
+ * take part in no conflict.  Results are the same either way (each item's
+ * arithmetic does not depend on the lane).
  * Errors: as crf_recompute_window; the failing item's index is in the message;
  * WORKSPACE if the second workspace cannot be allocated. */
 crf_status crf_recompute_window_batched(crf_context *ctx, const crf_model_dims *dims,

@@ -269,13 +269,6 @@ def kl_divergence(z_ref: np.ndarray, z: np.ndarray) -> float:
     return float(np.sum(np.exp(la) * (la - lb)))
 
 
-# ----------------------------------------------------------------------------- paging
-
-def paged_slot(t: int, block_table: Sequence[int], page_size: int) -> Tuple[int, int]:
-    """Physical (page, slot) of logical token t: page = table[t // page_size]."""
-    return int(block_table[t // page_size]), t % page_size
-
-
 # ----------------------------------------------------------------------------- drift
 
 def layer_drift(current: Sequence[LoraLayer], versions: Sequence[Sequence[LoraLayer]],

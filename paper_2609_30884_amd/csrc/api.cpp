@@ -131,7 +131,23 @@ crf_status check_dims(crf_context *ctx, const crf_model_dims *d) {
       return fail(ctx, CRF_ERR_UNSUPPORTED,
                   "bf16 path needs d_model, n_q_heads*head_dim, n_kv_heads*head_dim multiples of 128 and d_ffn a "
                   "multiple of 64");
+    // the projection kernels address each weight matrix through one buffer resource
+    // (the largest are [d_ffn, d_model] / [d_model, d_ffn] and [dq, d_model] / [d_model, dq])
+    if (std::max<int64_t>(d->d_ffn, dq_of(*d)) * d->d_model * 2 >= ((int64_t)1 << 31))
+      return fail(ctx, CRF_ERR_UNSUPPORTED, "bf16 path needs every projection weight smaller than 2 GiB");
   }
+  return CRF_OK;
+}
+
+// bf16 projections read their input [rows, K] through one buffer resource:
+// rows * max(d_model, n_q_heads*head_dim, d_ffn) * 2 bytes must stay below 2 GiB.
+crf_status check_gemm_rows(crf_context *ctx, const crf_model_dims *d, int64_t rows, const char *what) {
+  if (d->dtype != CRF_BF16 || rows <= 16) return CRF_OK;  // up to 16 rows take the weight-streaming kernels
+  const int64_t k = std::max<int64_t>(d->d_ffn, std::max<int64_t>(d->d_model, dq_of(*d)));
+  if (rows * k * 2 >= ((int64_t)1 << 31))
+    return fail(ctx, CRF_ERR_UNSUPPORTED,
+                "%s: %lld token rows x %lld features of bf16 projection input reach 2 GiB (at most %lld rows)", what,
+                (long long)rows, (long long)k, (long long)((((int64_t)1 << 31) - 1) / (2 * k)));
   return CRF_OK;
 }
 
@@ -164,11 +180,14 @@ bool same_dims(const crf_model_dims &a, const crf_model_dims &b) {
 }
 
 // Full validation of one window request against a context (host only).
+// gemm_rows: token rows the projections run over (the window's n_tokens, or a
+// decoding step's new tokens).
 crf_status check_request(crf_context *ctx, const crf_model_dims *dims, const void *hb,
                          const crf_layer_weights *w, const crf_lora_layer *lora, int32_t l0, int32_t h,
-                         const crf_kv_cache *kv, const void *hout, const char *what) {
+                         const crf_kv_cache *kv, const void *hout, const char *what, int64_t gemm_rows) {
   crf_status st = check_window(ctx, dims, l0, h, kv);
   if (st != CRF_OK) return st;
+  if (h > 0 && (st = check_gemm_rows(ctx, dims, gemm_rows, what)) != CRF_OK) return st;
   if (!same_dims(*dims, ctx->dims)) return fail(ctx, CRF_ERR_INVALID_ARG, "%s: dims differ from the context's", what);
   if (h == 0 || kv->n_tokens == 0) return CRF_OK;
   if (kv->n_tokens > ctx->max_tokens)
@@ -301,6 +320,7 @@ crf_status run_layers_bf16(crf_context *ctx, const void *hb, const crf_layer_wei
       p.kpad = rp;
       p.rank = rank;
       p.rope_cs = ctx->rope_cs;
+      p.q_scale = attn_query_scale(hd);
       p.pos0 = pos0;
       p.split_part = ctx->gemm_part;
       p.split_cap = ctx->gemm_part_floats;
@@ -539,7 +559,9 @@ const char *crf_last_error(const crf_context *ctx) { return ctx ? ctx->last_erro
 crf_status crf_validate_dims(const crf_model_dims *dims) { return check_dims(nullptr, dims); }
 
 crf_status crf_validate_window(const crf_model_dims *dims, int32_t l0, int32_t h, const crf_kv_cache *kv) {
-  return check_window(nullptr, dims, l0, h, kv);
+  crf_status st = check_window(nullptr, dims, l0, h, kv);
+  if (st == CRF_OK && h > 0) st = check_gemm_rows(nullptr, dims, kv->n_tokens, "crf_validate_window");
+  return st;
 }
 
 void crf_context_destroy(crf_context *ctx) {
@@ -635,7 +657,7 @@ crf_status crf_recompute_window(crf_context *ctx, const crf_model_dims *dims, co
                                 int32_t h, const crf_kv_cache *kv_cache, void *hidden_out, void *stream) {
   if (!ctx) return fail(nullptr, CRF_ERR_INVALID_ARG, "context is NULL");
   crf_status st = check_request(ctx, dims, hidden_at_boundary, base_weights, lora, l0, h, kv_cache, hidden_out,
-                                "crf_recompute_window");
+                                "crf_recompute_window", kv_cache ? kv_cache->n_tokens : 0);
   if (st != CRF_OK) return st;
   return run_window(ctx, hidden_at_boundary, base_weights, lora, l0, h, kv_cache, hidden_out, (hipStream_t)stream);
 }
@@ -650,7 +672,7 @@ crf_status crf_recompute_window_batched(crf_context *ctx, const crf_model_dims *
     snprintf(what, sizeof what, "item %d", i);
     const crf_window_item &it = items[i];
     crf_status st = check_request(ctx, dims, it.hidden_at_boundary, base_weights, it.lora, it.l0, it.h, &it.kv,
-                                  it.hidden_out, what);
+                                  it.hidden_out, what, it.kv.n_tokens);
     if (st != CRF_OK) return st;
   }
   // Independent items (no item writes a buffer that another reads or writes)
@@ -658,13 +680,38 @@ crf_status crf_recompute_window_batched(crf_context *ctx, const crf_model_dims *
   // windows fill the GPU together; every item's arithmetic is the same either
   // way.  While event timing is on they run in order on `stream`.
   bool lanes = n_items >= 2 && ctx->timer.mask == 0;
+  // Byte ranges each item may write (its window's layers of both pools, its
+  // output state) and read (the same pool layers, its boundary state, its
+  // block table).  Pages are chosen by device-side block tables, so a pool's
+  // range spans every page of the window's layers.
+  struct Span {
+    uintptr_t lo, hi;
+  };
+  auto overlap = [](Span a, Span b) { return a.lo < b.hi && b.lo < a.hi; };
+  std::vector<std::vector<Span>> wr(n_items), rd(n_items);
+  for (int i = 0; lanes && i < n_items; ++i) {
+    const crf_window_item &it = items[i];
+    if (it.h == 0 || it.kv.n_tokens == 0) continue;  // launches nothing
+    const size_t esz = ctx->esz;
+    const size_t row = (size_t)ctx->dims.d_model * esz * it.kv.n_tokens;
+    for (void *pool : {it.kv.k_pool, it.kv.v_pool}) {
+      const uintptr_t b = (uintptr_t)pool + (size_t)it.l0 * it.kv.layer_stride * esz;
+      const Span sp{b, b + ((size_t)(it.h - 1) * it.kv.layer_stride + (size_t)it.kv.n_pages * it.kv.page_stride) * esz};
+      wr[i].push_back(sp);
+      rd[i].push_back(sp);
+    }
+    if (it.hidden_out) wr[i].push_back(Span{(uintptr_t)it.hidden_out, (uintptr_t)it.hidden_out + row});
+    rd[i].push_back(Span{(uintptr_t)it.hidden_at_boundary, (uintptr_t)it.hidden_at_boundary + row});
+    const size_t bt = ((size_t)it.kv.n_tokens + it.kv.page_size - 1) / it.kv.page_size * sizeof(int32_t);
+    rd[i].push_back(Span{(uintptr_t)it.kv.block_table, (uintptr_t)it.kv.block_table + bt});
+  }
   for (int i = 0; lanes && i < n_items; ++i)
     for (int j = 0; lanes && j < n_items; ++j) {
       if (i == j) continue;
-      const crf_window_item &a = items[i], &b = items[j];
-      if (a.kv.k_pool == b.kv.k_pool || a.kv.v_pool == b.kv.v_pool || a.kv.k_pool == b.kv.v_pool)
-        lanes = false;
-      if (a.hidden_out && (a.hidden_out == b.hidden_out || a.hidden_out == b.hidden_at_boundary)) lanes = false;
+      for (const Span &w : wr[i]) {
+        for (const Span &o : wr[j]) lanes = lanes && !overlap(w, o);
+        for (const Span &o : rd[j]) lanes = lanes && !overlap(w, o);
+      }
     }
   if (!lanes) {
     for (int i = 0; i < n_items; ++i) {
@@ -730,7 +777,7 @@ crf_status crf_decode_logits(crf_context *ctx, const crf_model_dims *dims, const
   crf_kv_cache ext = *kv_cache;
   ext.n_tokens = kv_cache->n_tokens + n_new;
   crf_status st = check_request(ctx, dims, new_tokens, base_weights, lora, 0, ctx->dims.n_layers, &ext, nullptr,
-                                what);
+                                what, n_new);
   if (st != CRF_OK) return st;
   if (n_new > ctx->max_tokens)
     return fail(ctx, CRF_ERR_WORKSPACE, "%s: n_new %d exceeds the context's max_tokens", what, n_new);

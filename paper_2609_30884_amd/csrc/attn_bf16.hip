@@ -21,9 +21,17 @@
 //
 // The workgroup's page bases are staged in LDS once (validated there); a key
 // past the prefix or on a rejected page gets an out-of-range buffer offset,
-// which the hardware returns as zero.  The running max is only moved (and O
-// rescaled) when a score exceeds it by more than 2^8 in probability, so most
-// tiles skip the rescale; probabilities stay below 2^8.
+// which the hardware returns as zero.
+//
+// Online softmax without a per-block maximum: the query rows come scaled by
+// log2(e)/sqrt(hd) (attn_query_scale, applied where Q is stored) and each S
+// accumulator starts at -ref, the lane's current reference, so the MFMAs hand
+// back scores in log2 units already shifted and the probabilities are plain
+// exp2 of the accumulators.  The reference is the row maximum of the first
+// key block and is raised only when a half-block's probabilities sum past
+// 2^8, which bounds every probability by 2^8; only then is the block maximum
+// formed and O rescaled.  The result is the softmax of the definition (the
+// reference cancels between O and the row sum).
 //
 // Launch order: workgroup b runs on XCD b % 8.  When the KV-head count divides
 // 8, each XCD serves one KV head and every R-th query block (R = 8 / n_kv),
@@ -33,6 +41,7 @@
 #include <math.h>
 
 #include <algorithm>
+#include <type_traits>
 
 #include "kernels.hpp"
 
@@ -41,7 +50,7 @@ namespace {
 
 constexpr int BQ = 128;   // queries per workgroup
 constexpr int BKV = 64;   // keys per tile
-constexpr float RESCALE_THRESHOLD = 8.0f;  // log2 units
+constexpr float PSUM_MAX = 256.0f;  // bound on a half-block's probability sum (and each probability)
 constexpr int PGCAP = 2048;  // page bases staged in LDS at a time
 constexpr int SPLIT_WG = 1024;  // workgroups aimed at when a few query rows are split over the keys
 
@@ -230,10 +239,17 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16 *__restric
   for (int b = 0; b < HB; ++b)
 #pragma unroll
     for (int v = 0; v < 16; ++v) oacc[b][v] = 0.f;
-  // finite floor instead of -inf: a split may see no visible key for a row,
-  // and exp2(score - floor) of a masked score is still 0
-  float m_run = -1e30f, l_run = 0.f;
-  const float c2 = 1.4426950408889634f / sqrtf((float)HD);  // log2(e) / sqrt(hd)
+  // Scores arrive in log2 units (the query rows are stored pre-multiplied by
+  // log2(e)/sqrt(hd)) and relative to the lane's reference `ref`: the S
+  // accumulators start at -ref (negm), so exp2 of an accumulator is the
+  // probability up to the common factor 2^ref.  The reference is set to the
+  // row maximum on the wave's first key block and afterwards only raised,
+  // when the probabilities of a 32-key half-block sum past PSUM_MAX (which
+  // bounds each of them); most half-blocks therefore need no maximum at all.
+  float ref = 0.f, l_run = 0.f;
+  f32x16 negm;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) negm[v] = 0.f;
 
   // Transpose-read coordinates: 16-lane group gq covers hd 16*(gq&1) .. +15 of a
   // 32-row block and key rows 4*(gq>>1) + r; lane 4r + c reads hd chunk c*4.
@@ -242,8 +258,11 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16 *__restric
   const int tr_hd = 16 * (tr_g & 1) + 4 * tr_c;         // + 32*b
 
   // One tile: wait for its loads, publish them, start the next tile's loads
-  // into the other stage, then compute.
-  auto tile = [&](int it, const bf16 *kt, const bf16 *vt, bf16 *kn, bf16 *vn) {
+  // into the other stage, then compute.  FIRST: the range's first tile, where
+  // the reference is set (a row that sees any key of the range sees that
+  // tile's first key, which lies in its first half-block).
+  auto tile = [&](int it, const bf16 *kt, const bf16 *vt, bf16 *kn, bf16 *vn, auto first_t) {
+    constexpr bool FIRST = decltype(first_t)::value;
     const int kt0 = it * BKV;
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
@@ -258,10 +277,6 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16 *__restric
     // every key of this tile is in this wave's future, or every row of the wave is padding
     if (kt0 > pos_hi || q0w >= n_rows) return;
     f32x16 sacc[2];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) sacc[kb][v] = 0.f;
     // K fragments are read two k-steps ahead of the MFMAs that use them (the
     // scheduling barriers keep the compiler from regrouping them)
     bf16x8 kf[3][2];
@@ -279,7 +294,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16 *__restric
       if (s + 2 < KS) kread(s + 2, kf[(s + 2) % 3]);
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) sacc[kb] = mfma32(kf[s % 3][kb], qf[s], sacc[kb]);
+      for (int kb = 0; kb < 2; ++kb) sacc[kb] = mfma32(kf[s % 3][kb], qf[s], s == 0 ? negm : sacc[kb]);
       __builtin_amdgcn_sched_barrier(0);
     }
     // causal mask (also hides keys >= M, which are always > q_off + qrow for a valid row)
@@ -292,58 +307,76 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16 *__restric
           if (key > q_off + qrow) sacc[kb][v] = -INFINITY;
         }
     }
-    float mx = -INFINITY;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+    for (int kb = 0; kb < 2; ++kb) {
+      float pr[16];
+      float psum = 0.f;
 #pragma unroll
-      for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sacc[kb][v]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * c2;
-    // move the reference max only when a probability would exceed 2^8
-    const bool grow = mx > m_run + RESCALE_THRESHOLD;
-    if (__builtin_amdgcn_ballot_w64(grow)) {
-      const float m_new = grow ? mx : m_run;
-      const float alpha = fast_exp2(m_run - m_new);  // 0 on the first visible tile
-      m_run = m_new;
-      l_run *= alpha;
+      for (int v = 0; v < 16; ++v) {
+        pr[v] = fast_exp2(sacc[kb][v]);
+        psum += pr[v];
+      }
+      // (the negated test also catches an infinite sum)
+      if ((FIRST && kb == 0) || __builtin_amdgcn_ballot_w64(!(psum <= PSUM_MAX))) {
+        float mx = -INFINITY;
 #pragma unroll
-      for (int b = 0; b < HB; ++b) oacc[b] *= alpha;
-    }
-    float psum = 0.f;
-    bf16x8 pf[2][2];
+        for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sacc[kb][v]);
+        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+        float shift;
+        if (FIRST && kb == 0) {
+          // the reference jumps to the row maximum (a row that sees no key
+          // here sees none of the range: it keeps l = 0)
+          shift = mx > -INFINITY ? mx : 0.f;
+        } else {
+          shift = fmaxf(mx, 0.f);
+          const float alpha = fast_exp2(-shift);
+          l_run *= alpha;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+          for (int b = 0; b < HB; ++b) oacc[b] *= alpha;
+        }
+        ref += shift;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) negm[v] = -ref;
+#pragma unroll
+        for (int k2 = kb; k2 < 2; ++k2)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) sacc[k2][v] -= shift;
+        psum = 0.f;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          pr[v] = fast_exp2(sacc[kb][v]);
+          psum += pr[v];
+        }
+      }
+      l_run += psum;
+      bf16x8 pf[2];
 #pragma unroll
       for (int hh = 0; hh < 2; ++hh)
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float p = fast_exp2(fmaf(sacc[kb][8 * hh + e], c2, -m_run));
-          psum += p;
-          pf[kb][hh][e] = f2bf(p);
-        }
-    l_run += psum;
-    // O^T[hd, q] += V^T[hd, keys] P^T[keys, q]
+        for (int e = 0; e < 8; ++e) pf[hh][e] = f2bf(pr[8 * hh + e]);
+      // O^T[hd, q] += V^T[hd, keys] P^T[keys, q]
 #pragma unroll
-    for (int b = 0; b < HB; ++b) {
-      const int hd = 32 * b + tr_hd;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+      for (int b = 0; b < HB; ++b) {
+        const int hd = 32 * b + tr_hd;
 #pragma unroll
         for (int hh = 0; hh < 2; ++hh) {
           const int r0 = kb * 32 + 16 * hh + tr_key, r1 = r0 + 8;
           const s16x4 lo = ld_tr(vt + r0 * HD + vslot<HD>(r0, hd / 8) * 8 + hd % 8);
           const s16x4 hi = ld_tr(vt + r1 * HD + vslot<HD>(r1, hd / 8) * 8 + hd % 8);
           const s16x4 lohi[2] = {lo, hi};
-          oacc[b] = mfma32(__builtin_bit_cast(bf16x8, lohi), pf[kb][hh], oacc[b]);
+          oacc[b] = mfma32(__builtin_bit_cast(bf16x8, lohi), pf[hh], oacc[b]);
         }
+      }
     }
   };
 
   fill_pages(t_begin * BKV / ps);
   __syncthreads();
   dma(t_begin * BKV, ks0, vs0);
-  for (int it = t_begin; it < t_end; it += 2) {
-    tile(it, ks0, vs0, ks1, vs1);
-    if (it + 1 < t_end) tile(it + 1, ks1, vs1, ks0, vs0);
+  tile(t_begin, ks0, vs0, ks1, vs1, std::true_type());
+  for (int it = t_begin + 1; it < t_end; it += 2) {
+    tile(it, ks1, vs1, ks0, vs0, std::false_type());
+    if (it + 1 < t_end) tile(it + 1, ks0, vs0, ks1, vs1, std::false_type());
   }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
@@ -357,7 +390,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16 *__restric
         *reinterpret_cast<f32x4 *>(prow + b * 32 + 8 * ii + 4 * g) =
             f32x4{oacc[b][ii * 4], oacc[b][ii * 4 + 1], oacc[b][ii * 4 + 2], oacc[b][ii * 4 + 3]};
     if (g == 0) {
-      prow[HD] = m_run;
+      prow[HD] = l_tot > 0.f ? ref : -1e30f;  // a row that saw no key weighs 0 in the merge
       prow[HD + 1] = l_tot;
     }
     return;

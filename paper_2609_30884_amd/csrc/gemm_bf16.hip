@@ -570,6 +570,11 @@ __global__ __launch_bounds__(64 * WAVES, 1) void gemm_bf16_kernel(const GemmPara
               bf16 *dst;
               if (sg == 0) {
                 dst = p.q_out + (int64_t)m * p.dq + (head0 + hh) * HD;
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj) {
+                  x1[jj] *= p.q_scale;
+                  x2[jj] *= p.q_scale;
+                }
               } else {
                 if (prow[hh] < 0) continue;
                 dst = (bf16 *)(sg == 1 ? p.kv.k : p.kv.v) + prow[hh];
@@ -666,6 +671,8 @@ __global__ __launch_bounds__(256) void qkv_split_reduce_kernel(const GemmParams 
   bf16 *dst;
   if (sg == 0) {
     dst = p.q_out + (int64_t)m * p.dq + head * HD;
+    x1 *= p.q_scale;
+    x2 *= p.q_scale;
   } else {
     const int64_t prow = paged_row(p.kv, p.pos0 + m, head, HD);
     if (prow < 0) return;

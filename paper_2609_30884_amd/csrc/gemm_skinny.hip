@@ -171,6 +171,8 @@ __global__ void qkv_post_bf16_kernel(const GemmParams p, int hd) {
   bf16 *dst;
   if (seg == 0) {
     dst = p.q_out + (int64_t)m * p.dq + (int64_t)hl * hd;
+    x1 *= p.q_scale;
+    x2 *= p.q_scale;
   } else {
     const int64_t r = paged_row(p.kv, p.pos0 + m, hl, hd);
     if (r < 0) return;

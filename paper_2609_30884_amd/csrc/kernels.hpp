@@ -67,6 +67,7 @@ struct GemmParams {
   const bf16 *bias[3];
   bf16 *q_out;
   int dq;
+  float q_scale;               // factor applied to Q (after bias and rotary) before it is stored
   PagedKV kv;
   const float2 *rope_cs;
   // EPI_QKV: token row m sits at position pos0 + m (rotary angle and page slot)
@@ -117,7 +118,11 @@ hipError_t launch_gemm_dn_sum(hipStream_t s, const GemmParams &p, bf16 *U, int l
 // The same projections for M <= 16 token rows (weight-streaming bound).
 hipError_t launch_gemm_skinny_bf16(hipStream_t s, GemmEpi epi, int hd, const GemmParams &p);
 
-// Query rows 0..Mq-1 at positions q_off..q_off+Mq-1 over keys 0..q_off+Mq-1.
+// Factor the attention kernel expects the stored query rows to carry:
+// log2(e) / sqrt(head_dim) (scores then come out in log2 units).
+inline float attn_query_scale(int hd) { return 1.4426950408889634f / __builtin_sqrtf((float)hd); }
+// Query rows 0..Mq-1 at positions q_off..q_off+Mq-1 over keys 0..q_off+Mq-1,
+// Q pre-multiplied by attn_query_scale(hd).
 // part (nullable, part_floats floats): workspace for splitting a few query
 // rows (<= 16) over the keys of a long prefix.
 hipError_t launch_attn_bf16(hipStream_t s, const bf16 *Q, const PagedKV &kv, bf16 *O, int Mq, int q_off, int nq,

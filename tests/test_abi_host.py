@@ -133,3 +133,28 @@ def test_timing_classes_rejects_null_context():
     lib = crf.load()
     assert lib.crf_context_set_timing_classes(None, 1) == 1  # CRF_ERR_INVALID_ARG
     assert lib.crf_context_set_timing(None, 1) == 1
+
+
+Q7 = dict(n_layers=28, d_model=3584, n_q_heads=28, n_kv_heads=4, head_dim=128, d_ffn=18944)
+
+
+def test_validate_window_rejects_projection_inputs_of_2gib():
+    """At 7B shapes the down projection's input [n, d_ffn] bf16 reaches 2 GiB at
+    n = 56,680 tokens: such a request is refused before anything is launched
+    (the projection kernels address their input through one buffer resource)."""
+    d = dims(**Q7)
+    limit = ((1 << 31) - 1) // (2 * 18944)
+    assert limit == 56679
+    pages = (60000 + 15) // 16
+    assert crf.validate_window(d, 14, 2, kv(n_tokens=60000, n_pages=pages, nkv=4)) == 4
+    assert "2 GiB" in crf.last_error()
+    assert crf.validate_window(d, 14, 2, kv(n_tokens=limit, n_pages=pages, nkv=4)) == 0
+    assert crf.validate_window(d, 14, 2, kv(n_tokens=limit + 1, n_pages=pages, nkv=4)) == 4
+    assert crf.validate_window(d, 14, 0, kv(n_tokens=60000, n_pages=pages, nkv=4)) == 0  # h = 0: reuse
+    assert crf.validate_window(dims(**Q7, dtype="f32"), 14, 2,
+                               kv(n_tokens=60000, n_pages=pages, nkv=4)) == 0  # fp32 path: 64-bit indexing
+
+
+def test_validate_dims_rejects_projection_weights_of_2gib():
+    assert crf.validate_dims(dims(d_model=8192, d_ffn=131072, n_q_heads=64, n_kv_heads=8)) == 4
+    assert crf.validate_dims(dims(d_model=8192, d_ffn=65536, n_q_heads=64, n_kv_heads=8)) == 0
