@@ -2,6 +2,9 @@
 and run the oracle on the same host values."""
 from __future__ import annotations
 
+import json
+import os
+
 import numpy as np
 
 import synthetic as syn
@@ -9,12 +12,29 @@ import synthetic as syn
 # Per output tensor T (each refreshed layer's K and V, and the window output):
 #   rms-relative error      ||T_gpu - T_ref||_2 / ||T_ref||_2
 #   element max-rel-to-RMS  max_i |T_gpu,i - T_ref,i| / rms(T_ref)
-# fp32: both <= 1e-4.  bf16: rms-relative <= 2e-2; the element metric is bounded
-# by what ideal bf16 execution reaches on these workloads (an exact CPU model of
-# bf16 storage with fp32 accumulation gives up to 3.2e-2 on a two-layer 7B
-# window), with headroom: 6e-2 for windows of up to three layers.
+# against the fp64 oracle.  fp32: both <= 1e-4.  bf16: each metric <= the
+# larger of 2e-2 and MODEL_HEADROOM times what ideal bf16 execution reaches
+# on the same inputs (tests/golden/bf16_model.py: fp32 arithmetic with every
+# bf16-stored tensor rounded where the kernels store it).  Rounding a stored
+# bf16 tensor alone costs up to 2^-8 max|T| / rms(T) per element, about 2e-2
+# on the large tensors, so the element bound follows the model; the relative
+# RMS error of ideal execution stays below 2e-2 for windows of up to three
+# layers, where the bound is 2e-2.
 TOL = {"f32": 1e-4, "bf16": 2e-2}
-TOL_ELEM = {"f32": 1e-4, "bf16": 6e-2}
+MODEL_HEADROOM = 1.5
+MODEL_RUNS = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "bf16_model_errors.json")
+
+
+def stored_model_elem_max() -> float:
+    """Largest element error of ideal bf16 execution over the stored runs of
+    windows of up to three layers (the 1.5B 4K and 7B 16K windows)."""
+    runs = json.load(open(MODEL_RUNS))
+    return max(e["elem"] for r in runs.values() if r["h"] <= 3 for e in r["errors"].values())
+
+
+# per-element bound where no model run is made (decoding steps, the mixed batch):
+# the largest stored ideal-bf16 element error times the headroom
+TOL_ELEM = {"f32": 1e-4, "bf16": MODEL_HEADROOM * stored_model_elem_max()}
 
 
 def rel_to_rms(got, ref) -> float:
@@ -76,11 +96,24 @@ def gpu_kv(case, layer, rows=None):
             gather_kv(case.v_pool, layer, case.block_table, n, case.wl.page_size, rows))
 
 
+def model_window(case):
+    """The ideal-bf16 execution model over the case's window and inputs."""
+    from tests.golden.bf16_model import _bf16, model_layer
+    win = case.window
+    cur = np.asarray(case.hidden, np.float32)
+    kv = {}
+    for l in range(win.l0, win.l0 + win.h):
+        cur, k, v = model_layer(cur, case.weights[l], case.lora.get(l), case.dims, case.wl.lora_scale)
+        kv[l] = (k, v)
+    return _bf16(cur), kv
+
+
 def assert_window_parity(case, out_ref, kv_ref, tol=None, tol_elem=None, label=""):
-    """Element-by-element parity of every refreshed K/V layer and hidden_out."""
+    """Element-by-element parity of every refreshed K/V layer and hidden_out.
+
+    bf16 windows are bounded through the ideal-bf16 model run on the same
+    inputs (see TOL); explicit tol / tol_elem override the bounds."""
     dt = case.dims.dtype
-    tol = TOL[dt] if tol is None else tol
-    tol_elem = TOL_ELEM[dt] if tol_elem is None else tol_elem
     pairs = {}
     for l, (k_ref, v_ref) in kv_ref.items():
         k, v = gpu_kv(case, l)
@@ -88,8 +121,21 @@ def assert_window_parity(case, out_ref, kv_ref, tol=None, tol_elem=None, label="
         pairs[f"V{l}"] = (v, v_ref)
     pairs["hidden_out"] = (case.hidden_out.float().cpu().numpy(), out_ref)
     errs = {k: (rms_rel(g, r), rel_to_rms(g, r)) for k, (g, r) in pairs.items()}
-    print(f"[parity] {label} (rms-rel, elem) " + " ".join(f"{k}=({a:.2e},{b:.2e})" for k, (a, b) in errs.items()),
-          flush=True)
-    bad = {k: v for k, v in errs.items() if not (v[0] <= tol and v[1] <= tol_elem)}
-    assert not bad, f"{label}: errors above ({tol}, {tol_elem}): {bad}"
+    bounds = {k: (TOL[dt], TOL[dt]) for k in pairs}
+    if dt == "bf16" and (tol is None or tol_elem is None):
+        assert sorted(kv_ref) == list(range(case.window.l0, case.window.l0 + case.window.h))
+        m_out, m_kv = model_window(case)
+        model = {"hidden_out": (m_out, out_ref)}
+        for l, (k_ref, v_ref) in kv_ref.items():
+            model[f"K{l}"] = (m_kv[l][0], k_ref)
+            model[f"V{l}"] = (m_kv[l][1], v_ref)
+        for k, (g, r) in model.items():
+            bounds[k] = (max(TOL[dt], MODEL_HEADROOM * rms_rel(g, r)), max(TOL[dt], MODEL_HEADROOM * rel_to_rms(g, r)))
+    if tol is not None or tol_elem is not None:
+        bounds = {k: (tol if tol is not None else b[0], tol_elem if tol_elem is not None else b[1])
+                  for k, b in bounds.items()}
+    print(f"[parity] {label} (rms-rel, elem / elem bound) " +
+          " ".join(f"{k}=({a:.2e},{b:.2e}/{bounds[k][1]:.2e})" for k, (a, b) in errs.items()), flush=True)
+    bad = {k: (v, bounds[k]) for k, v in errs.items() if not (v[0] <= bounds[k][0] and v[1] <= bounds[k][1])}
+    assert not bad, f"{label}: errors above their bounds: {bad}"
     return {k: v[0] for k, v in errs.items()}

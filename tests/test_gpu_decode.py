@@ -15,10 +15,13 @@ SMALL = dict(n_layers=4, d_model=768, n_q_heads=12, n_kv_heads=2, head_dim=64, d
 VOCAB = 1024
 
 
-def _setup(seed, n, m, base="qwen15b_4k", shape=SMALL, vocab=VOCAB):
+def _setup(seed, n, m, base="qwen15b_4k", shape=SMALL, vocab=VOCAB, page_size=None):
+    import dataclasses
     from oracle import oracle as O
     from synthetic.device import build_case, scatter_kv, to_dev
     wl = syn.WORKLOADS[base].with_dims(**shape).with_window(n_tokens=n + m, l0=0, h=shape["n_layers"])
+    if page_size is not None:
+        wl = dataclasses.replace(wl, page_size=page_size)
     dims = wl.dims
     N = dims.n_layers
     case = build_case(wl, seed, lora_version=3, layers=range(N))         # current adapter: version 3
@@ -67,6 +70,25 @@ SPLIT_CASES = {
 def test_decode_key_split_shapes(name):
     base, shape, n, m, vocab = SPLIT_CASES[name]
     _check_decode(11, n, m, 1, base=base, shape=shape, vocab=vocab)
+
+
+# More than 16 new tokens take the window kernels with a position offset: the
+# projection epilogue rotates and pages row r at position n + r, and attention
+# runs query blocks at that offset over the prefix and the rows before them.
+MANY_CASES = {
+    "m40": (300, 40, None),
+    "m257": (500, 257, None),
+    # one-token pages: the page bases of a 2600-token prefix exceed what a
+    # workgroup stages at once (key-split attention refills them mid-range)
+    "m3_pages1": (2600, 3, 1),
+    "m40_pages1": (2300, 40, 1),
+}
+
+
+@pytest.mark.parametrize("name", list(MANY_CASES))
+def test_decode_many_new_tokens_and_page_refill(name):
+    n, m, ps = MANY_CASES[name]
+    _check_decode(13, n, m, 2, page_size=ps)
 
 
 def _check_decode(seed, n, m, b, **kw):

@@ -122,6 +122,10 @@ def test_bf16_window_parity(name, n, seed):
     (8, 128, 12, 2, 700),    # runtime page size; two KV heads (four XCDs per KV head)
     (1, 64, 12, 6, 300),     # one-token pages, head_dim 64, six KV heads (plain launch order)
     (32, 64, 8, 2, 1100),    # 32-token pages, head_dim 64
+    # one-token pages past the 2048 page bases a workgroup stages at a time:
+    # the later query blocks refill their page bases mid-way
+    (1, 128, 8, 2, 2500),
+    (1, 64, 12, 6, 4200),
 ])
 def test_bf16_page_sizes_and_head_shapes(page_size, hd, nq, nkv, n):
     """Paged attention and the K/V-writing epilogue with page sizes other than
