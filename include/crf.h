@@ -268,6 +268,29 @@ crf_status crf_layer_drift(crf_context *ctx, const crf_model_dims *dims, const c
                            const int32_t *anchor_version, const float *sensitivity, int32_t per_layer_only,
                            float *drift_out, float *risk_out, float *sq_partial_out, void *stream);
 
+/* crf_layer_drift for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc).
+ * Same arguments and results as crf_layer_drift (bitwise: the same kernels in
+ * the same order) without a context: the segment tables and the partial sums
+ * live in a fixed device scratch of CRF_DRIFT_NOALLOC_MAX_BYTES that the
+ * library holds on each device it runs on until the process ends, and the
+ * tables are staged on the host in a fixed per-thread buffer of the same size.
+ * Nothing is allocated on the device and no allocating library routine is
+ * called; the tables reach the scratch by one hipMemcpyAsync from pageable host
+ * memory on `stream` (so the call returns once they are copied).  Calls that
+ * overlap on one device race on its scratch: serialise them (one stream, or
+ * the caller's own ordering).  A request whose tables and partials exceed the
+ * scratch (segments: two per adapter target, layer and version; chunks of 2^16
+ * elements each; about 64 bytes per chunk and segment) is rejected with
+ * WORKSPACE before anything is copied or launched.  Errors are reported through
+ * crf_last_error(NULL): INVALID_ARG, SHAPE, UNSUPPORTED (as crf_validate_dims),
+ * WORKSPACE, HIP. */
+#define CRF_DRIFT_NOALLOC_MAX_BYTES (4 << 20)
+crf_status crf_layer_drift_noalloc(const crf_model_dims *dims, const crf_lora_layer *current, int32_t n_versions,
+                                   const crf_lora_layer *const *versions, const int32_t *anchor_version,
+                                   const float *sensitivity, int32_t per_layer_only, float *drift_out,
+                                   float *risk_out, float *sq_partial_out, void *stream);
+
 /* Device-side error flags raised by kernels' own bounds checks since the last
  * call (bit 0: a block table entry outside [0, n_pages)).  Synchronises the
  * device, then clears the flags. */

@@ -70,7 +70,7 @@ EXPORTS = ("crf_status_string", "crf_abi_version", "crf_context_create", "crf_co
            "crf_validate_dims", "crf_validate_window", "crf_recompute_window", "crf_recompute_window_batched",
            "crf_layer_drift", "crf_context_device_errors", "crf_context_set_timing", "crf_context_set_timing_classes",
            "crf_context_read_timing",
-           "crf_device_info", "crf_decode_logits")
+           "crf_device_info", "crf_decode_logits", "crf_layer_drift_noalloc")
 
 
 def load(path: str = LIB_PATH) -> ctypes.CDLL:
@@ -103,6 +103,9 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.crf_layer_drift.restype = I32
     lib.crf_layer_drift.argtypes = [VP, P(ModelDims), P(LoraLayer), I32, P(P(LoraLayer)), P(I32), VP, I32, VP, VP,
                                     VP, VP]
+    lib.crf_layer_drift_noalloc.restype = I32
+    lib.crf_layer_drift_noalloc.argtypes = [P(ModelDims), P(LoraLayer), I32, P(P(LoraLayer)), P(I32), VP, I32, VP,
+                                            VP, VP, VP]
     lib.crf_context_device_errors.restype = I32
     lib.crf_context_device_errors.argtypes = [VP, P(I32)]
     lib.crf_context_set_timing.restype = I32
@@ -322,3 +325,17 @@ def layer_drift(ctx: Context, dims: ModelDims, current: ctypes.Array, versions: 
                                  1 if per_layer_only else 0, _ptr(drift_out), _ptr(risk_out), _ptr(sq_partial_out),
                                  _stream(stream))
     _err(ctx.lib, ctx.handle, st)
+
+
+def layer_drift_noalloc(dims: ModelDims, current: ctypes.Array, versions: Sequence[ctypes.Array],
+                        anchor_version: Sequence[int], sensitivity, drift_out, risk_out, sq_partial_out=None,
+                        per_layer_only: bool = False, stream=None):
+    """crf_layer_drift_noalloc: crf_layer_drift without a context, in the library's fixed device scratch."""
+    lib = load()
+    n_layers = dims.n_layers
+    vp = (ctypes.POINTER(LoraLayer) * len(versions))(*[ctypes.cast(v, ctypes.POINTER(LoraLayer)) for v in versions])
+    anc = (ctypes.c_int32 * n_layers)(*[int(a) for a in anchor_version])
+    st = lib.crf_layer_drift_noalloc(ctypes.byref(dims), current, len(versions), vp, anc, _ptr(sensitivity),
+                                     1 if per_layer_only else 0, _ptr(drift_out), _ptr(risk_out),
+                                     _ptr(sq_partial_out), _stream(stream))
+    _err(lib, None, st)

@@ -536,6 +536,112 @@ crf_status dmalloc(crf_context *ctx, T **p, size_t bytes) {
 
 }  // namespace
 
+namespace {
+
+// Drift tables: segments (one per current/version factor pair), chunks of at
+// most 2^16 elements, and per (version, layer) the first chunk and the chunk
+// count.  Staging layout: segs | chunks | first | count | anchor, copied from
+// the host, then partials (double, one per chunk) and scratch (double, one per
+// (version, layer)) written by the kernels.
+constexpr int64_t DRIFT_CHUNK = 1 << 16;
+
+struct DriftPlan {
+  int L = 0, V = 0;
+  size_t n_segs = 0, n_chunks = 0;
+  size_t o_segs = 0, o_chunks = 0, o_first = 0, o_count = 0, o_anchor = 0, host_bytes = 0, o_part = 0, o_scr = 0,
+         dev_bytes = 0;
+};
+
+// Validates a drift request and sizes its tables (touches no device).
+crf_status drift_plan(crf_context *ctx, const crf_model_dims *dims, const crf_lora_layer *current, int32_t n_versions,
+                      const crf_lora_layer *const *versions, const int32_t *anchor_version, const float *drift_out,
+                      const float *risk_out, DriftPlan &pl) {
+  if (!current || !versions || !anchor_version || !drift_out || !risk_out || n_versions < 1)
+    return fail(ctx, CRF_ERR_INVALID_ARG, "NULL argument or n_versions < 1");
+  const int L = dims->n_layers;
+  for (int l = 0; l < L; ++l)
+    if (anchor_version[l] < 0 || anchor_version[l] >= n_versions)
+      return fail(ctx, CRF_ERR_INVALID_ARG, "anchor_version[%d] = %d outside [0, %d)", l, anchor_version[l],
+                  n_versions);
+  pl = DriftPlan{};
+  pl.L = L;
+  pl.V = n_versions;
+  for (int v = 0; v < n_versions; ++v) {
+    if (!versions[v]) return fail(ctx, CRF_ERR_INVALID_ARG, "versions[%d] is NULL", v);
+    for (int l = 0; l < L; ++l) {
+      const crf_lora_layer &c = current[l], &vv = versions[v][l];
+      for (int t = 0; t < CRF_NUM_TARGETS && c.rank > 0; ++t) {
+        if (!c.A[t]) continue;
+        if (!c.B[t] || !vv.A[t] || !vv.B[t] || vv.rank != c.rank)
+          return fail(ctx, CRF_ERR_INVALID_ARG, "layer %d target %d missing or rank differs in version %d", l, t, v);
+        int d_out, d_in;
+        target_shape(*dims, t, d_out, d_in);
+        const int64_t cnt[2] = {(int64_t)c.rank * d_in, (int64_t)d_out * c.rank};
+        for (int k = 0; k < 2; ++k) {
+          ++pl.n_segs;
+          pl.n_chunks += (size_t)((cnt[k] + DRIFT_CHUNK - 1) / DRIFT_CHUNK);
+        }
+      }
+    }
+  }
+  auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
+  const size_t n_out = (size_t)n_versions * L;
+  pl.o_segs = 0;
+  pl.o_chunks = al(pl.o_segs + pl.n_segs * sizeof(DriftSeg));
+  pl.o_first = al(pl.o_chunks + pl.n_chunks * sizeof(DriftChunk));
+  pl.o_count = al(pl.o_first + n_out * sizeof(int));
+  pl.o_anchor = al(pl.o_count + n_out * sizeof(int));
+  pl.host_bytes = al(pl.o_anchor + L * sizeof(int));
+  pl.o_part = pl.host_bytes;
+  pl.o_scr = al(pl.o_part + (pl.n_chunks + 1) * sizeof(double));
+  pl.dev_bytes = al(pl.o_scr + n_out * sizeof(double));
+  return CRF_OK;
+}
+
+// Writes the tables of a planned request into host staging hb (host_bytes).
+void drift_fill(const DriftPlan &pl, const crf_model_dims *dims, const crf_lora_layer *current,
+                const crf_lora_layer *const *versions, const int32_t *anchor_version, char *hb) {
+  DriftSeg *segs = (DriftSeg *)(hb + pl.o_segs);
+  DriftChunk *chunks = (DriftChunk *)(hb + pl.o_chunks);
+  int *first = (int *)(hb + pl.o_first), *count = (int *)(hb + pl.o_count);
+  int ns = 0, nc = 0;
+  for (int v = 0; v < pl.V; ++v)
+    for (int l = 0; l < pl.L; ++l) {
+      const int o = v * pl.L + l;
+      first[o] = nc;
+      const crf_lora_layer &c = current[l], &vv = versions[v][l];
+      for (int t = 0; t < CRF_NUM_TARGETS && c.rank > 0; ++t) {
+        if (!c.A[t]) continue;
+        int d_out, d_in;
+        target_shape(*dims, t, d_out, d_in);
+        const int64_t cnt[2] = {(int64_t)c.rank * d_in, (int64_t)d_out * c.rank};
+        const void *pa[2] = {c.A[t], c.B[t]}, *pb[2] = {vv.A[t], vv.B[t]};
+        for (int k = 0; k < 2; ++k) {
+          const int si = ns++;
+          segs[si] = DriftSeg{pa[k], pb[k], cnt[k], o};
+          for (int64_t s0 = 0; s0 < cnt[k]; s0 += DRIFT_CHUNK)
+            chunks[nc++] = DriftChunk{si, s0, std::min(DRIFT_CHUNK, cnt[k] - s0)};
+        }
+      }
+      count[o] = nc - first[o];
+    }
+  memcpy(hb + pl.o_anchor, anchor_version, pl.L * sizeof(int));
+}
+
+// The two drift kernels over staging db (tables already there).
+hipError_t drift_launch(hipStream_t s, const DriftPlan &pl, char *db, bool f32, const float *sensitivity,
+                        int32_t per_layer_only, float *drift_out, float *risk_out, float *sq_partial_out) {
+  hipError_t e = launch_drift_partials(s, (const DriftSeg *)(db + pl.o_segs), (const DriftChunk *)(db + pl.o_chunks),
+                                       (int)pl.n_chunks, f32, (double *)(db + pl.o_part));
+  if (e != hipSuccess) return e;
+  return launch_drift_finalize(s, (const double *)(db + pl.o_part), (const int *)(db + pl.o_first),
+                               (const int *)(db + pl.o_count), pl.V, pl.L, (const int *)(db + pl.o_anchor),
+                               sensitivity, per_layer_only, drift_out, risk_out, sq_partial_out,
+                               (double *)(db + pl.o_scr));
+}
+
+}  // namespace
+
 extern "C" {
 
 const char *crf_status_string(crf_status s) {
@@ -820,85 +926,66 @@ crf_status crf_layer_drift(crf_context *ctx, const crf_model_dims *dims, const c
   crf_status st = check_dims(ctx, dims);
   if (st != CRF_OK) return st;
   if (!same_dims(*dims, ctx->dims)) return fail(ctx, CRF_ERR_INVALID_ARG, "dims differ from the context's");
-  if (!current || !versions || !anchor_version || !drift_out || !risk_out || n_versions < 1)
-    return fail(ctx, CRF_ERR_INVALID_ARG, "NULL argument or n_versions < 1");
-  const int L = dims->n_layers;
-  for (int l = 0; l < L; ++l)
-    if (anchor_version[l] < 0 || anchor_version[l] >= n_versions)
-      return fail(ctx, CRF_ERR_INVALID_ARG, "anchor_version[%d] = %d outside [0, %d)", l, anchor_version[l],
-                  n_versions);
-  const int64_t CH = 1 << 16;
-  std::vector<DriftSeg> segs;
-  std::vector<DriftChunk> chunks;
-  std::vector<int> first(n_versions * L), count(n_versions * L);
-  for (int v = 0; v < n_versions; ++v) {
-    if (!versions[v]) return fail(ctx, CRF_ERR_INVALID_ARG, "versions[%d] is NULL", v);
-    for (int l = 0; l < L; ++l) {
-      const int o = v * L + l;
-      first[o] = (int)chunks.size();
-      const crf_lora_layer &c = current[l], &vv = versions[v][l];
-      for (int t = 0; t < CRF_NUM_TARGETS && c.rank > 0; ++t) {
-        if (!c.A[t]) continue;
-        if (!c.B[t] || !vv.A[t] || !vv.B[t] || vv.rank != c.rank)
-          return fail(ctx, CRF_ERR_INVALID_ARG, "layer %d target %d missing or rank differs in version %d", l, t, v);
-        int d_out, d_in;
-        target_shape(*dims, t, d_out, d_in);
-        const int64_t na = (int64_t)c.rank * d_in, nb = (int64_t)d_out * c.rank;
-        const void *pa[2] = {c.A[t], c.B[t]}, *pb[2] = {vv.A[t], vv.B[t]};
-        const int64_t cnt[2] = {na, nb};
-        for (int k = 0; k < 2; ++k) {
-          const int si = (int)segs.size();
-          segs.push_back(DriftSeg{pa[k], pb[k], cnt[k], o});
-          for (int64_t s0 = 0; s0 < cnt[k]; s0 += CH) chunks.push_back(DriftChunk{si, s0, std::min(CH, cnt[k] - s0)});
-        }
-      }
-      count[o] = (int)chunks.size() - first[o];
-    }
-  }
-  // staging layout: segs | chunks | first | count | anchor | partials(double) | scratch(double)
-  auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
-  const size_t o_segs = 0, o_chunks = al(o_segs + segs.size() * sizeof(DriftSeg));
-  const size_t o_first = al(o_chunks + chunks.size() * sizeof(DriftChunk));
-  const size_t o_count = al(o_first + first.size() * sizeof(int));
-  const size_t o_anchor = al(o_count + count.size() * sizeof(int));
-  const size_t host_bytes = al(o_anchor + L * sizeof(int));
-  const size_t o_part = host_bytes, o_scr = al(o_part + (chunks.size() + 1) * sizeof(double));
-  const size_t dev_bytes = al(o_scr + first.size() * sizeof(double));
+  DriftPlan pl;
+  if ((st = drift_plan(ctx, dims, current, n_versions, versions, anchor_version, drift_out, risk_out, pl)) != CRF_OK)
+    return st;
   hipStream_t s = (hipStream_t)stream;
   if (!ctx->drift_ev) HIP_TRY(ctx, hipEventCreateWithFlags(&ctx->drift_ev, hipEventDisableTiming));
   if (ctx->drift_ev_recorded) HIP_TRY(ctx, hipEventSynchronize(ctx->drift_ev));
-  if (host_bytes > ctx->drift_host_bytes) {
+  if (pl.host_bytes > ctx->drift_host_bytes) {
     if (ctx->drift_host) HIP_TRY(ctx, hipHostFree(ctx->drift_host));
     ctx->drift_host = nullptr;
     ctx->drift_host_bytes = 0;
-    HIP_TRY(ctx, hipHostMalloc(&ctx->drift_host, host_bytes, hipHostMallocDefault));
-    ctx->drift_host_bytes = host_bytes;
+    HIP_TRY(ctx, hipHostMalloc(&ctx->drift_host, pl.host_bytes, hipHostMallocDefault));
+    ctx->drift_host_bytes = pl.host_bytes;
   }
-  if (dev_bytes > ctx->drift_dev_bytes) {
+  if (pl.dev_bytes > ctx->drift_dev_bytes) {
     HIP_TRY(ctx, hipStreamSynchronize(s));
     if (ctx->drift_dev) HIP_TRY(ctx, hipFree(ctx->drift_dev));
     ctx->drift_dev = nullptr;
     ctx->drift_dev_bytes = 0;
-    HIP_TRY(ctx, hipMalloc(&ctx->drift_dev, dev_bytes));
-    ctx->drift_dev_bytes = dev_bytes;
+    HIP_TRY(ctx, hipMalloc(&ctx->drift_dev, pl.dev_bytes));
+    ctx->drift_dev_bytes = pl.dev_bytes;
   }
   char *hb = (char *)ctx->drift_host, *db = (char *)ctx->drift_dev;
-  memcpy(hb + o_segs, segs.data(), segs.size() * sizeof(DriftSeg));
-  memcpy(hb + o_chunks, chunks.data(), chunks.size() * sizeof(DriftChunk));
-  memcpy(hb + o_first, first.data(), first.size() * sizeof(int));
-  memcpy(hb + o_count, count.data(), count.size() * sizeof(int));
-  memcpy(hb + o_anchor, anchor_version, L * sizeof(int));
-  HIP_TRY(ctx, hipMemcpyAsync(db, hb, host_bytes, hipMemcpyHostToDevice, s));
+  drift_fill(pl, dims, current, versions, anchor_version, hb);
+  HIP_TRY(ctx, hipMemcpyAsync(db, hb, pl.host_bytes, hipMemcpyHostToDevice, s));
   HIP_TRY(ctx, hipEventRecord(ctx->drift_ev, s));
   ctx->drift_ev_recorded = true;
-  const bool f32 = dims->dtype == CRF_F32;
   LAUNCH(ctx, s, CRF_KK_DRIFT,
-         launch_drift_partials(s, (const DriftSeg *)(db + o_segs), (const DriftChunk *)(db + o_chunks),
-                               (int)chunks.size(), f32, (double *)(db + o_part)));
-  LAUNCH(ctx, s, CRF_KK_DRIFT,
-         launch_drift_finalize(s, (const double *)(db + o_part), (const int *)(db + o_first),
-                               (const int *)(db + o_count), n_versions, L, (const int *)(db + o_anchor), sensitivity,
-                               per_layer_only, drift_out, risk_out, sq_partial_out, (double *)(db + o_scr)));
+         drift_launch(s, pl, db, dims->dtype == CRF_F32, sensitivity, per_layer_only, drift_out, risk_out,
+                      sq_partial_out));
+  return CRF_OK;
+}
+
+crf_status crf_layer_drift_noalloc(const crf_model_dims *dims, const crf_lora_layer *current, int32_t n_versions,
+                                   const crf_lora_layer *const *versions, const int32_t *anchor_version,
+                                   const float *sensitivity, int32_t per_layer_only, float *drift_out,
+                                   float *risk_out, float *sq_partial_out, void *stream) {
+  crf_status st = check_dims(nullptr, dims);
+  if (st != CRF_OK) return st;
+  DriftPlan pl;
+  if ((st = drift_plan(nullptr, dims, current, n_versions, versions, anchor_version, drift_out, risk_out, pl)) !=
+      CRF_OK)
+    return st;
+  if (pl.dev_bytes > CRF_DRIFT_NOALLOC_MAX_BYTES)
+    return fail(nullptr, CRF_ERR_WORKSPACE,
+                "crf_layer_drift_noalloc: %zu segments in %zu chunks need %zu bytes of scratch, more than its %d",
+                pl.n_segs, pl.n_chunks, pl.dev_bytes, CRF_DRIFT_NOALLOC_MAX_BYTES);
+  void *scratch = nullptr;
+  hipError_t e = drift_noalloc_scratch(&scratch);
+  if (e != hipSuccess)
+    return fail(nullptr, CRF_ERR_HIP, "crf_layer_drift_noalloc: scratch address: %s", hipGetErrorString(e));
+  // host staging of the tables: one fixed buffer per host thread
+  static thread_local char hstage[CRF_DRIFT_NOALLOC_MAX_BYTES];
+  drift_fill(pl, dims, current, versions, anchor_version, hstage);
+  hipStream_t s = (hipStream_t)stream;
+  // a copy from pageable memory has read the source when it returns
+  e = hipMemcpyAsync(scratch, hstage, pl.host_bytes, hipMemcpyHostToDevice, s);
+  if (e == hipSuccess)
+    e = drift_launch(s, pl, (char *)scratch, dims->dtype == CRF_F32, sensitivity, per_layer_only, drift_out,
+                     risk_out, sq_partial_out);
+  if (e != hipSuccess) return fail(nullptr, CRF_ERR_HIP, "crf_layer_drift_noalloc: %s", hipGetErrorString(e));
   return CRF_OK;
 }
 

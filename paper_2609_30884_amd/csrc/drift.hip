@@ -3,7 +3,15 @@
 // reduced in a fixed order (deterministic).  Accumulation in fp64.
 #include <math.h>
 
+#include <mutex>
+
+#include "../../include/crf.h"
 #include "kernels.hpp"
+
+// Fixed device scratch of crf_layer_drift_noalloc (tables and partials), one
+// copy per device, held until the process ends.  Host code never passes this
+// name to a kernel: the device address comes from hipGetSymbolAddress.
+static __device__ __align__(256) char scratch[CRF_DRIFT_NOALLOC_MAX_BYTES];
 
 namespace crf {
 namespace {
@@ -70,7 +78,27 @@ __global__ __launch_bounds__(256) void drift_finalize_kernel(const double *__res
   }
 }
 
+constexpr int MAX_DEVICES = 64;
+void *g_scratch[MAX_DEVICES];
+std::once_flag g_scratch_once[MAX_DEVICES];
+hipError_t g_scratch_err[MAX_DEVICES];
+
 }  // namespace
+
+hipError_t drift_noalloc_scratch(void **out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= MAX_DEVICES) return hipErrorInvalidDevice;
+  // once per device, with that device current (it is: hipGetDevice above)
+  std::call_once(g_scratch_once[dev], [dev] {
+    void *p = nullptr;
+    g_scratch_err[dev] = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    g_scratch[dev] = g_scratch_err[dev] == hipSuccess ? p : nullptr;
+  });
+  *out = g_scratch[dev];
+  return g_scratch_err[dev];
+}
 
 hipError_t launch_drift_partials(hipStream_t s, const DriftSeg *segs, const DriftChunk *chunks, int n_chunks,
                                  bool f32, double *partials) {

@@ -141,6 +141,9 @@ struct DriftChunk {
 };
 hipError_t launch_drift_partials(hipStream_t s, const DriftSeg *segs, const DriftChunk *chunks, int n_chunks,
                                  bool f32, double *partials);
+// Device address of the no-allocation drift scratch on the current device
+// (CRF_DRIFT_NOALLOC_MAX_BYTES, looked up once per device).
+hipError_t drift_noalloc_scratch(void **out);
 hipError_t launch_drift_finalize(hipStream_t s, const double *partials, const int *chunk_first,
                                  const int *chunk_count, int n_versions, int n_layers, const int *anchor,
                                  const float *sens, int per_layer_only, float *drift, float *risk, float *sq_out,

@@ -158,3 +158,25 @@ def test_validate_window_rejects_projection_inputs_of_2gib():
 def test_validate_dims_rejects_projection_weights_of_2gib():
     assert crf.validate_dims(dims(d_model=8192, d_ffn=131072, n_q_heads=64, n_kv_heads=8)) == 4
     assert crf.validate_dims(dims(d_model=8192, d_ffn=65536, n_q_heads=64, n_kv_heads=8)) == 0
+
+
+def test_drift_noalloc_rejects_requests_beyond_its_scratch():
+    """The no-allocation drift call refuses, before any device work, a request
+    whose tables and partials do not fit its fixed scratch (here 7B shapes,
+    rank 64 on all seven targets, 64 stored versions)."""
+    lib = crf.load()
+    d = dims(**Q7)
+    L = d.n_layers
+    fake = 1 << 20  # the pointers are never dereferenced by the host checks
+    lay = (crf._lib.LoraLayer * L)()
+    for l in range(L):
+        lay[l].rank, lay[l].scale = 64, 1.0
+        for t in range(7):
+            lay[l].A[t] = fake
+            lay[l].B[t] = fake
+    V = 64
+    vp = (ctypes.POINTER(crf._lib.LoraLayer) * V)(*[ctypes.cast(lay, ctypes.POINTER(crf._lib.LoraLayer))] * V)
+    anc = (ctypes.c_int32 * L)(*([0] * L))
+    st = lib.crf_layer_drift_noalloc(ctypes.byref(d), lay, V, vp, anc, None, 0, fake, fake, None, None)
+    assert st == 5 and "scratch" in crf.last_error()
+    assert lib.crf_layer_drift_noalloc(ctypes.byref(d), None, V, vp, anc, None, 0, fake, fake, None, None) == 1
