@@ -94,9 +94,10 @@ def kernel_flops(dims, n, rank, targets):
     }
 
 
-def cpu_baseline(case, n_sample: int):
-    """The oracle (fp64 numpy) on the first n_sample prefix tokens of the same
-    window; returns token-layers/s, seconds and thread count."""
+def cpu_baseline(case, n_layers: int):
+    """The oracle (fp64 numpy) over the whole prefix of the same window, for
+    its first n_layers layers; returns token-layers/s, seconds, BLAS threads
+    and the BLAS name."""
     import numpy as np
     from oracle import oracle as O
     blas = "unknown"
@@ -109,11 +110,10 @@ def cpu_baseline(case, n_sample: int):
     except Exception:
         threads = len(os.sched_getaffinity(0))
     win = case.window
-    h0 = case.hidden[:n_sample]
     t0 = time.perf_counter()
-    O.recompute_window(h0, case.weights, case.lora, win.l0, win.h, case.dims, case.wl.lora_scale)
+    O.recompute_window(case.hidden, case.weights, case.lora, win.l0, n_layers, case.dims, case.wl.lora_scale)
     dt = time.perf_counter() - t0
-    return n_sample * win.h / dt, dt, threads, blas
+    return win.n_tokens * n_layers / dt, dt, threads, blas
 
 
 def cpu_model() -> str:
@@ -160,8 +160,12 @@ def main():
     ap.add_argument("--workload", default="qwen7b_16k")
     ap.add_argument("--seed", type=int, default=7)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample-tokens", type=int, default=8192)
+    ap.add_argument("--cpu-sample-layers", type=int, default=1,
+                    help="window layers the CPU oracle runs over the whole prefix (bounded CPU time)")
     ap.add_argument("--updates", type=int, default=32, help="trajectory workload: number of adapter updates")
+    ap.add_argument("--restart-every", type=int, default=1,
+                    help="trajectory workload: retained boundary states every k layers (windows run as one call "
+                         "per span between them)")
     ap.add_argument("--no-hidden-out", action="store_true",
                     help="window without hidden_out: the last layer runs its K/V projections only")
     args = ap.parse_args()
@@ -299,13 +303,15 @@ def main():
         "device": device,
     }
     if not args.no_cpu_baseline:
-        ns = min(args.cpu_sample_tokens, win.n_tokens)
-        print(f"[bench] cpu baseline: oracle on {ns} tokens ...", file=sys.stderr, flush=True)
-        v, dt, thr, blas = cpu_baseline(case, ns)
+        nl = max(1, min(args.cpu_sample_layers, win.h))
+        print(f"[bench] cpu baseline: oracle over {win.n_tokens} tokens, {nl} layer(s) ...", file=sys.stderr,
+              flush=True)
+        v, dt, thr, blas = cpu_baseline(case, nl)
+        layers = f"layer {win.l0}" if nl == 1 else f"layers [{win.l0},{win.l0 + nl})"
         out["cpu_baseline"] = {
             "value": round(v, 1), "unit": "token-layers/s", "cores": thr, "kind": "oracle",
-            "sample": f"fp64 numpy oracle, first {ns} of {win.n_tokens} prefix tokens through layers "
-                      f"[{win.l0},{win.l0 + win.h}) ({dt:.1f} s; causal attention over that shorter prefix)",
+            "sample": f"fp64 numpy oracle, {layers} of the window [{win.l0},{win.l0 + win.h}) over all "
+                      f"{win.n_tokens} of {win.n_tokens} prefix tokens (full causal attention; {dt:.1f} s)",
             "cpu": cpu_model(), "blas": blas,
         }
     print(json.dumps(out), flush=True)
@@ -457,9 +463,10 @@ def bench_trajectory(args):
     adapters = AdapterVersions(setup.base_lora)
     keep, states = [], {}
     for name in ("fresh", "suffix", "policy"):
-        k, v, bnd = make_state_buffers(setup, wl.page_size)
+        k, v, bnd = make_state_buffers(setup, wl.page_size, args.restart_every)
         keep.append((k, v, bnd))
-        states[name] = CacheState(crf.kv_cache(k, v, setup.block_table, n, wl.page_size), bnd)
+        states[name] = CacheState(crf.kv_cache(k, v, setup.block_table, n, wl.page_size), bnd,
+                                  restart_every=args.restart_every)
     stream = torch.cuda.current_stream()
     ex = Executor(ctx, cd, weights, stream)
     for st in states.values():   # every copy starts as a fresh prefill under version 0
@@ -488,7 +495,8 @@ def bench_trajectory(args):
            "higher_is_better": False, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
            "data": "synthetic (seeded device draws; one B factor moves by N(0,0.005) per update)",
            "config": {"workload": f"trajectory: {len(setup.updates)} updates, Qwen2.5-7B shapes, {n}-token prefix, "
-                                  f"{dims.n_layers} layers, LoRA rank {wl.lora_rank} on {','.join(wl.lora_targets)}",
+                                  f"{dims.n_layers} layers, LoRA rank {wl.lora_rank} on {','.join(wl.lora_targets)}, "
+                                  f"boundary states retained every {args.restart_every} layer(s)",
                       "updates": [f"{t}@{l}" for l, t in setup.updates]},
            "strategies": summ,
            "sensitivity": [round(float(x), 4) for x in sens.cpu()]}

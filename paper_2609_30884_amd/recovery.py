@@ -11,9 +11,17 @@ H_{l-1} let any layer be a restart point.  Per update and strategy:
            recompute [r, b_t) with b_t = 1 + max{q_l >= 1} (Eq. 9), or reuse;
 * reuse    keep the cache (no maintenance).
 
-Only recomputed layers move their anchors to the current version.  Windows
-run one layer per call so that every boundary state they produce is retained
-for later restarts; the compute is crf_recompute_window / crf_layer_drift.
+Only recomputed layers move their anchors to the current version.
+
+Restart boundaries (Sec. 4.2: a restart at r needs the retained state H_{r-1})
+are kept every `restart_every` layers (boundaries[l] for l a multiple of it;
+1 = every layer).  A restart is rounded down to the nearest retained boundary
+(the layers in between see unchanged inputs and weights, so their refreshed
+K/V equal the cached ones), and a window runs as one crf_recompute_window call
+per span between retained boundaries: the span's output goes to the next
+retained boundary, and a span that ends at the window end off a boundary runs
+without an output state (its last layer needs only its K/V projections).  The
+compute is crf_recompute_window / crf_layer_drift.
 """
 from __future__ import annotations
 
@@ -72,15 +80,35 @@ class AdapterVersions:
 @dataclass
 class CacheState:
     """One maintained prefix: paged K/V of every layer (kv), the retained
-    boundary states (boundaries[l] = H_{l-1}, boundaries[0] = H_{-1}) and the
-    per-layer anchor versions."""
+    boundary states (boundaries[l] = H_{l-1}, boundaries[0] = H_{-1}; None
+    where l is not a multiple of restart_every), the per-layer anchor
+    versions and the spacing of the retained boundaries."""
     kv: object
     boundaries: list
     anchor: np.ndarray = field(default=None)
+    restart_every: int = 1
 
     def __post_init__(self):
         if self.anchor is None:
             self.anchor = np.zeros(len(self.boundaries) - 1, dtype=np.int32)
+        if self.restart_every < 1:
+            raise ValueError("restart_every must be >= 1")
+
+    def restart(self, r: Optional[int]) -> Optional[int]:
+        """The retained boundary a restart at layer r starts from."""
+        return None if r is None else r - r % self.restart_every
+
+    def spans(self, r: int, b: int):
+        """(start, end, output boundary index or None) of the calls covering [r, b)."""
+        k = self.restart_every
+        if r % k:
+            raise ValueError(f"restart {r} is not a retained boundary (every {k} layers)")
+        out, l = [], r
+        while l < b:
+            e = min(l + k, b)
+            out.append((l, e, e if (e % k == 0 or e == len(self.boundaries) - 1) else None))
+            l = e
+        return out
 
 
 @dataclass
@@ -102,9 +130,9 @@ class Executor:
         self.ctx, self.dims, self.weights, self.stream = ctx, dims, weights, stream
 
     def recompute(self, state: CacheState, lora_array, r: int, b: int):
-        for l in range(r, b):
-            L.recompute_window(self.ctx, self.dims, state.boundaries[l], self.weights, lora_array, l, 1, state.kv,
-                               state.boundaries[l + 1], self.stream)
+        for l0, e, out in state.spans(r, b):
+            L.recompute_window(self.ctx, self.dims, state.boundaries[l0], self.weights, lora_array, l0, e - l0,
+                               state.kv, None if out is None else state.boundaries[out], self.stream)
 
     def risk(self, adapters: AdapterVersions, anchor: np.ndarray, sensitivity, drift_out, risk_out) -> np.ndarray:
         used = sorted(set(int(a) for a in anchor))
@@ -138,8 +166,9 @@ class RecoveryLoop:
         n, v = self.n, upd.version
         arr = self.adapters.array(v)
         out = []
-        r = executable_restart(upd.target, upd.layer, n)
+        r_exec = executable_restart(upd.target, upd.layer, n)
         for name, st in self.states.items():
+            r = st.restart(r_exec) if st is not None else r_exec
             if name == "fresh":
                 dt = self._timed(lambda: self.ex.recompute(st, arr, 0, n))
                 st.anchor[:] = v

@@ -94,14 +94,16 @@ def new_b(setup: TrajectorySetup, lora_now: List[dict], layer: int, target: str,
     return (b.float() + 0.005 * torch.randn(b.shape, generator=g, device="cuda")).to(torch.bfloat16).contiguous()
 
 
-def make_state_buffers(setup: TrajectorySetup, page_size: int):
-    """Paged K/V pools (canary-filled) and one boundary-state buffer per layer
-    boundary (boundaries[0] holds H_{-1})."""
+def make_state_buffers(setup: TrajectorySetup, page_size: int, restart_every: int = 1):
+    """Paged K/V pools (canary-filled) and a boundary-state buffer at every
+    retained boundary: boundaries[0] holds H_{-1}, boundaries[l] exists for l a
+    multiple of restart_every and for l = N (the last layer's output)."""
     d = setup.dims
     shape = (d.n_layers, setup.n_phys, d.n_kv_heads, page_size, d.head_dim)
     k = torch.empty(shape, dtype=torch.bfloat16, device="cuda")
     v = torch.empty(shape, dtype=torch.bfloat16, device="cuda")
     canary_fill(k)
     canary_fill(v)
-    bnd = [setup.embedding] + [torch.empty_like(setup.embedding) for _ in range(d.n_layers)]
+    bnd = [setup.embedding] + [torch.empty_like(setup.embedding) if (l % restart_every == 0 or l == d.n_layers)
+                               else None for l in range(1, d.n_layers + 1)]
     return k, v, bnd

@@ -78,3 +78,37 @@ def test_unknown_strategy_rejected():
     loop = RecoveryLoop(ex, FakeAdapters(), {"bogus": None}, N, sensitivity=None)
     with pytest.raises(ValueError):
         loop.step(Update(1, 0, "q"))
+
+
+def test_retained_boundaries_spans_and_restarts():
+    """With a retained state every k layers, a restart rounds down to a
+    retained boundary and a window runs as one call per span between them; a
+    span ending at the window end off a boundary writes no output state."""
+    st = CacheState(kv=None, boundaries=[None] * (N + 1), restart_every=3)
+    assert [st.restart(r) for r in range(N)] == [0, 0, 0, 3, 3, 3, 6, 6]
+    assert st.restart(None) is None
+    assert st.spans(0, N) == [(0, 3, 3), (3, 6, 6), (6, 8, 8)]      # layer N's output is retained
+    assert st.spans(3, 5) == [(3, 5, None)]
+    assert st.spans(3, 7) == [(3, 6, 6), (6, 7, None)]
+    with pytest.raises(ValueError):
+        st.spans(4, 6)
+    one = CacheState(kv=None, boundaries=[None] * (N + 1))
+    assert one.spans(2, 5) == [(2, 3, 3), (3, 4, 4), (4, 5, 5)]
+    with pytest.raises(ValueError):
+        CacheState(kv=None, boundaries=[None] * (N + 1), restart_every=0)
+
+
+def test_policy_restarts_from_retained_boundary():
+    s = np.zeros(N)
+    s[6] = 2.0
+    ex = FakeExecutor(s)
+    st = CacheState(kv=None, boundaries=[None] * (N + 1), restart_every=4)
+    ad = FakeAdapters()
+    loop = RecoveryLoop(ex, ad, {"policy": st, "suffix": CacheState(kv=None, boundaries=[None] * (N + 1),
+                                                                     restart_every=4)}, N, sensitivity=None)
+    ad.current = 1
+    recs = {r.strategy: r for r in loop.step(Update(1, 5, "v"))}
+    d = recs["policy"].decision
+    assert (d.action, d.r, d.b) == ("bounded", 4, 7)     # restart 5 rounds down to the boundary at 4
+    assert (recs["suffix"].r, recs["suffix"].b) == (4, N)
+    assert list(st.anchor) == [0, 0, 0, 0, 1, 1, 1, 0]
