@@ -48,7 +48,12 @@
 namespace crf {
 namespace {
 
-constexpr int BQ = 128;   // queries per workgroup
+#ifndef CRF_ATTN_WAVES
+#define CRF_ATTN_WAVES 4
+#endif
+constexpr int NW = CRF_ATTN_WAVES;  // waves per workgroup, 32 queries each
+constexpr int BQ = 32 * NW;         // queries per workgroup
+constexpr int NT = 64 * NW;         // threads per workgroup
 constexpr int BKV = 64;   // keys per tile
 constexpr float PSUM_MAX = 256.0f;  // bound on a half-block's probability sum (and each probability)
 constexpr int PGCAP = 2048;  // page bases staged in LDS at a time
@@ -95,7 +100,7 @@ struct PageMap {
 // PS: page size when fixed at compile time (16), 0 = runtime kv.page_size.
 // XCD: balanced per-XCD KV-head mapping (R = 8 / nkv XCDs per KV head).
 template <int HD, int PS>
-__global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16 *__restrict__ Q, PagedKV kv,
+__global__ __launch_bounds__(NT, 8 / NW) void attn_bf16_kernel(const bf16 *__restrict__ Q, PagedKV kv,
                                                            bf16 *__restrict__ O, int Mq, int q_off, int nq,
                                                            int nkv, uint32_t pool_bytes, int xcd_r,
                                                            int split_tiles, int packed, float *__restrict__ part) {
@@ -103,7 +108,8 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16 *__restric
   constexpr int KS = HD / 16;            // MFMA k-steps for S
   constexpr int HB = HD / 32;            // 32-row hd blocks of O^T
   constexpr int RPI = 64 / CH;           // rows per 64-lane load instruction
-  constexpr int IPW = BKV / RPI / 4;     // load instructions per wave per tile (each of K and V)
+  constexpr int RPW = BKV / NW;          // key rows each wave loads per tile
+  constexpr int IPW = RPW / RPI;         // load instructions per wave per tile (each of K and V)
   constexpr int TILE = BKV * HD;         // elements per K (or V) tile
   // one array per stage and operand, so the compiler sees that loads into one
   // stage never alias reads of the other
@@ -175,40 +181,41 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16 *__restric
   int pg_first = 0;
   auto fill_pages = [&](int first) {
     pg_first = first;
-    for (int i = tid; i < min(PGCAP, n_pages_needed - first); i += 256) pgbase[i] = pm.base(first + i);
+    for (int i = tid; i < min(PGCAP, n_pages_needed - first); i += NT) pgbase[i] = pm.base(first + i);
   };
 
   // This lane's row and chunk in each of the wave's load instructions.  A wave
-  // loads 16 consecutive rows (keys) of the tile; the in-page part of each
+  // loads RPW consecutive rows (keys) of the tile; the in-page part of each
   // lane's offset (row in the page, swizzled chunk) is fixed for the kernel
   // when the page size is a multiple of 16.
   const int lrow = lane / CH, lslot = lane % CH;
   uint32_t koff[IPW], voff[IPW];
 #pragma unroll
   for (int i = 0; i < IPW; ++i) {
-    const int row = RPI * i + lrow;  // row within the wave's 16
-    koff[i] = (uint32_t)(row * HD * 2 + kslot<HD>(row, lslot) * 16);
-    voff[i] = (uint32_t)(row * HD * 2 + vslot<HD>(row, lslot) * 16);
+    const int row = RPI * i + lrow;    // row within the wave's rows
+    const int trow = wave * RPW + row;  // row within the tile (the LDS swizzle's row)
+    koff[i] = (uint32_t)(row * HD * 2 + kslot<HD>(trow, lslot) * 16);
+    voff[i] = (uint32_t)(row * HD * 2 + vslot<HD>(trow, lslot) * 16);
   }
   auto dma = [&](int kt0, bf16 *kdst, bf16 *vdst) {
-    const int wrow0 = kt0 + wave * (BKV / 4);  // first key of this wave's 16 rows
+    const int wrow0 = kt0 + wave * RPW;  // first key of this wave's rows
     if (PS > 0 && PS % 16 == 0) {
-      // the wave's 16 rows share one page: one uniform base (CRF_OOB plus an
+      // the wave's rows share one page: one uniform base (CRF_OOB plus an
       // in-page offset stays out of range, pool sizes being below 2^31)
       const int pidx = min(max(wrow0 / PS - pg_first, 0), PGCAP - 1);
       const uint32_t b =
           (uint32_t)__builtin_amdgcn_readfirstlane((int)pgbase[pidx]) + (uint32_t)((wrow0 % PS) * HD * 2);
-      if (wrow0 + BKV / 4 <= M) {  // uniform: all 16 rows inside the prefix
+      if (wrow0 + RPW <= M) {  // uniform: all the wave's rows inside the prefix
 #pragma unroll
         for (int i = 0; i < IPW; ++i) {
-          const int ldsoff = (wave * (BKV / 4) + RPI * i) * HD;  // wave-uniform first row of this instruction
+          const int ldsoff = (wave * RPW + RPI * i) * HD;  // wave-uniform first row of this instruction
           dma16(kres, (lds_char *)(kdst + ldsoff), b + koff[i], 0);
           dma16(vres, (lds_char *)(vdst + ldsoff), b + voff[i], 0);
         }
       } else {
 #pragma unroll
         for (int i = 0; i < IPW; ++i) {
-          const int ldsoff = (wave * (BKV / 4) + RPI * i) * HD;
+          const int ldsoff = (wave * RPW + RPI * i) * HD;
           const bool in = wrow0 + RPI * i + lrow < M;
           dma16(kres, (lds_char *)(kdst + ldsoff), in ? b + koff[i] : CRF_OOB, 0);
           dma16(vres, (lds_char *)(vdst + ldsoff), in ? b + voff[i] : CRF_OOB, 0);
@@ -223,11 +230,11 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16 *__restric
       }
 #pragma unroll
       for (int i = 0; i < IPW; ++i) {
-        const int row = wave * (BKV / 4) + RPI * i + lrow;  // key within the tile
+        const int row = wave * RPW + RPI * i + lrow;  // key within the tile
         const int tok = kt0 + row;
         const bool ok = tok < M && b[i] != CRF_OOB;
         const uint32_t rowoff = b[i] + (uint32_t)((tok % ps) * HD * 2);
-        const int ldsoff = (wave * (BKV / 4) + RPI * i) * HD;
+        const int ldsoff = (wave * RPW + RPI * i) * HD;
         dma16(kres, (lds_char *)(kdst + ldsoff), ok ? rowoff + (uint32_t)(kslot<HD>(row, lslot) * 16) : CRF_OOB, 0);
         dma16(vres, (lds_char *)(vdst + ldsoff), ok ? rowoff + (uint32_t)(vslot<HD>(row, lslot) * 16) : CRF_OOB, 0);
       }
@@ -477,10 +484,10 @@ void launch(hipStream_t s, const bf16 *Q, const PagedKV &kv, bf16 *O, int Mq, in
   }
   const dim3 g3(grid, n_splits);
   if (kv.page_size == 16)
-    hipLaunchKernelGGL((attn_bf16_kernel<HD, 16>), g3, dim3(256), 0, s, Q, kv, O, Mq, q_off, nq, nkv, pool_bytes,
+    hipLaunchKernelGGL((attn_bf16_kernel<HD, 16>), g3, dim3(NT), 0, s, Q, kv, O, Mq, q_off, nq, nkv, pool_bytes,
                        xcd_r, split_tiles, packed, part);
   else
-    hipLaunchKernelGGL((attn_bf16_kernel<HD, 0>), g3, dim3(256), 0, s, Q, kv, O, Mq, q_off, nq, nkv, pool_bytes,
+    hipLaunchKernelGGL((attn_bf16_kernel<HD, 0>), g3, dim3(NT), 0, s, Q, kv, O, Mq, q_off, nq, nkv, pool_bytes,
                        xcd_r, split_tiles, packed, part);
   if (split_tiles > 0)
     hipLaunchKernelGGL((attn_merge_kernel<HD>), dim3(Mq * nq), dim3(256), 0, s, part, O, Mq, nq, n_splits);
