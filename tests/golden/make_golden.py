@@ -7,10 +7,11 @@ a fixed set of sampled token rows and the RMS of the whole tensor, so a GPU
 test can compute the element metric and the relative RMS error on the samples
 against the full-tensor RMS.
 
-    OPENBLAS_NUM_THREADS=6 python tests/golden/make_golden.py qwen7b_16k_suffix qwen15b_mixed8
+    OPENBLAS_NUM_THREADS=6 python tests/golden/make_golden.py qwen7b_16k_suffix
 
-(The 7B-shaped 16K window itself is compared on whole tensors against the
-oracle run next to the GPU, so it needs no stored samples.)
+(The 7B-shaped 16K window and the 8-item mixed batch are compared on whole
+tensors against the oracle run next to the GPU, so they need no stored
+samples.)
 """
 from __future__ import annotations
 
@@ -79,4 +80,4 @@ def main(names):
 
 
 if __name__ == "__main__":
-    main(sys.argv[1:] or ["qwen7b_16k_suffix", "qwen15b_mixed8"])
+    main(sys.argv[1:] or ["qwen7b_16k_suffix"])
