@@ -363,3 +363,72 @@ def test_batched_chained_items_run_in_order():
     crf.recompute_window(ctx, cd, mid2, w, las[1], 3, 1, kvs[1], cases[1].hidden_out)
     torch.cuda.synchronize()
     assert bits_equal(mid, mid2) and bits_equal(got, cases[1].hidden_out)
+
+
+def _run_pair(crf, ctx, cd, w, its, batched):
+    if batched:
+        crf.recompute_window_batched(ctx, cd, w, its)
+    else:
+        for it in its:
+            crf.recompute_window(ctx, cd, it.hidden_at_boundary, w, it.lora, it.l0, it.h, it.kv, it.hidden_out)
+    torch.cuda.synchronize()
+
+
+def test_batched_overlapping_views_run_in_order():
+    """Items that share memory through different views (no base pointer in
+    common) are not independent: (a) the second item's pools are the first's
+    shifted by one layer, so their windows [2, 4) and [1, 3) write the same two
+    layers; (b) the second item's boundary state starts 64 rows into the first
+    one's output.  Each batch must equal the two windows run in order,
+    bitwise."""
+    import paper_2609_30884_amd as crf
+    from synthetic.device import canary_fill
+    n = 300
+    base, cases = _batched_cases([syn.Window(n, 2, 2), syn.Window(n, 1, 2)])
+    cd = cdims(base.dims)
+    ctx = crf.Context(cd, n, base.lora_rank)
+    w = crf.layer_weights_array(cases[0].weights_dev)
+    las = [crf.lora_array(c.lora_dev, base.dims.n_layers) for c in cases]
+    a, b = cases
+    assert a.n_phys == b.n_phys
+    shape = (base.dims.n_layers + 1,) + tuple(a.k_pool.shape[1:])
+    kp = torch.empty(shape, dtype=a.k_pool.dtype, device="cuda")
+    vp = torch.empty_like(kp)
+
+    def pool_items():
+        canary_fill(kp)
+        canary_fill(vp)
+        kva = crf.kv_cache(kp[:-1], vp[:-1], a.block_table_dev, n, base.page_size)
+        kvb = crf.kv_cache(kp[1:], vp[1:], b.block_table_dev, n, base.page_size)
+        return [crf.window_item(a.hidden_dev, las[0], 2, 2, kva, a.hidden_out),
+                crf.window_item(b.hidden_dev, las[1], 1, 2, kvb, b.hidden_out)]
+
+    print("[case] batched items on layer-shifted views of one pool", flush=True)
+    _run_pair(crf, ctx, cd, w, pool_items(), batched=False)
+    ref = (kp.clone(), vp.clone(), b.hidden_out.clone())
+    _run_pair(crf, ctx, cd, w, pool_items(), batched=True)
+    assert ctx.device_errors() == 0
+    assert bits_equal(kp, ref[0]) and bits_equal(vp, ref[1]) and bits_equal(b.hidden_out, ref[2])
+
+    # (b) hidden-state overlap: b's boundary = rows [64, 64 + n) of a buffer whose rows [0, n) are a's output
+    buf = torch.empty((n + 64, base.dims.d_model), dtype=a.hidden_dev.dtype, device="cuda")
+
+    def hidden_items():
+        buf.zero_()
+        buf[n:] = b.hidden_dev[n - 64:]
+        canary_fill(a.k_pool)
+        canary_fill(b.k_pool)
+        canary_fill(a.v_pool)
+        canary_fill(b.v_pool)
+        kva = crf.kv_cache(a.k_pool, a.v_pool, a.block_table_dev, n, base.page_size)
+        kvb = crf.kv_cache(b.k_pool, b.v_pool, b.block_table_dev, n, base.page_size)
+        return [crf.window_item(a.hidden_dev, las[0], 2, 2, kva, buf[:n]),
+                crf.window_item(buf[64:], las[1], 1, 2, kvb, b.hidden_out)]
+
+    print("[case] batched item reading an overlapping part of another's output", flush=True)
+    _run_pair(crf, ctx, cd, w, hidden_items(), batched=False)
+    ref = (buf.clone(), b.k_pool.clone(), b.v_pool.clone(), b.hidden_out.clone())
+    _run_pair(crf, ctx, cd, w, hidden_items(), batched=True)
+    assert ctx.device_errors() == 0
+    assert (bits_equal(buf, ref[0]) and bits_equal(b.k_pool, ref[1]) and bits_equal(b.v_pool, ref[2])
+            and bits_equal(b.hidden_out, ref[3]))
