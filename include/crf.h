@@ -268,8 +268,10 @@ crf_status crf_layer_drift(crf_context *ctx, const crf_model_dims *dims, const c
                            const int32_t *anchor_version, const float *sensitivity, int32_t per_layer_only,
                            float *drift_out, float *risk_out, float *sq_partial_out, void *stream);
 
-/* crf_layer_drift for callers that cannot allocate device memory (code under
- * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc).
+/* crf_layer_drift for callers that cannot allocate device memory (tight
+ * serving loops, harnesses that forbid hipMalloc).  Not for stream capture:
+ * the tables are uploaded from a host buffer that the next call on the same
+ * thread overwrites, so a captured copy would read whatever it holds then.
  * Same arguments and results as crf_layer_drift (bitwise: the same kernels in
  * the same order) without a context: the segment tables and the partial sums
  * live in a fixed device scratch of CRF_DRIFT_NOALLOC_MAX_BYTES that the
