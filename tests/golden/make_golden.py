@@ -30,8 +30,8 @@ from oracle import oracle as O  # noqa: E402
 
 SEED = 7
 N_SAMPLES = 16
-# layers whose K/V are stored for the 24-layer suffix (first, last and a spread)
-SUFFIX_KV_LAYERS = (4, 5, 10, 16, 22, 27)
+# layers whose K/V are stored for the 24-layer suffix: all of them
+SUFFIX_KV_LAYERS = tuple(range(4, 28))
 
 
 def sample_rows(n: int) -> np.ndarray:

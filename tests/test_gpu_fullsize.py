@@ -122,7 +122,7 @@ def test_full_size_window_whole_tensors():
 
 def test_full_size_suffix_window():
     """The 24-layer suffix [4, 28) at 7B shapes and 16K tokens on stored
-    oracle rows (layers 4, 5, 10, 16, 22, 27 and the window output)."""
+    oracle rows (every refreshed layer's K and V and the window output)."""
     from synthetic.device import build_case
     from tests.helpers import run_gpu_window
     name = "qwen7b_16k_suffix"
