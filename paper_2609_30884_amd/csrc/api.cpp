@@ -344,9 +344,12 @@ crf_status run_layers_bf16(crf_context *ctx, const void *hb, const crf_layer_wei
     };
 
     // attention block
+    // the window's first O projection reads the bf16 boundary state as its old
+    // residual (the weight-streaming kernels of a few rows read the fp32 copy)
+    const bool resid_from_boundary = first && !skinny;
     LAUNCH(ctx, s, CRF_KK_NORM,
            launch_rmsnorm(s, first ? hb : (const void *)ctx->hres, !first, w.attn_norm, false, xn, false,
-                          first ? ctx->hres : nullptr, M, D, d.rms_eps));
+                          first && !resid_from_boundary ? ctx->hres : nullptr, M, D, d.rms_eps));
     if (last && !hout && kv_tail) {
       // Nothing reads this layer's output: its cache entry depends only on its
       // input through the K and V projections, so only those run.
@@ -411,6 +414,7 @@ crf_status run_layers_bf16(crf_context *ctx, const void *hb, const crf_layer_wei
         p.ucol[0] = 0;
       }
       p.resid = ctx->hres;
+      p.resid_in = resid_from_boundary ? (const bf16 *)hb : nullptr;
       p.ldr = D;
       LAUNCH(ctx, s, CRF_KK_GEMM_O, gemm(EPI_RESID, p));
     }

@@ -28,6 +28,11 @@ CRF_DEV void st16(void *p, u32x4 v) { *reinterpret_cast<u32x4 *>(p) = v; }
 CRF_DEV u32x2 ld8(const void *p) { return *reinterpret_cast<const u32x2 *>(p); }
 CRF_DEV void st8(void *p, u32x2 v) { *reinterpret_cast<u32x2 *>(p) = v; }
 
+// the 4 bf16 values of an 8-byte load as floats
+CRF_DEV f32x4 unpack_bf16x4(u32x2 v) {
+  return f32x4{__builtin_bit_cast(float, v[0] << 16), __builtin_bit_cast(float, v[0] & 0xffff0000u),
+               __builtin_bit_cast(float, v[1] << 16), __builtin_bit_cast(float, v[1] & 0xffff0000u)};
+}
 CRF_DEV u32x2 pack_bf16x4(float a, float b, float c, float d) {
   bf16x4 v = {f2bf(a), f2bf(b), f2bf(c), f2bf(d)};
   return __builtin_bit_cast(u32x2, v);

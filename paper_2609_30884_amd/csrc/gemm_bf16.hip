@@ -430,7 +430,9 @@ __global__ __launch_bounds__(64 * WAVES, 1) void gemm_bf16_kernel(const GemmPara
             const int n = n0 + wn * 128 + 32 * ii + 8 * q + 4 * g;
             if (n >= p.N) continue;
             float *rp = p.resid + (int64_t)m * p.ldr + n;
-            f32x4 r = p.resid_overwrite ? f32x4{0.f, 0.f, 0.f, 0.f} : *reinterpret_cast<f32x4 *>(rp);
+            f32x4 r = p.resid_overwrite ? f32x4{0.f, 0.f, 0.f, 0.f}
+                      : p.resid_in      ? unpack_bf16x4(ld8(p.resid_in + (int64_t)m * p.ldr + n))
+                                        : *reinterpret_cast<f32x4 *>(rp);
 #pragma unroll
             for (int jj = 0; jj < 4; ++jj) r[jj] += acc[ii][j][q * 4 + jj];
             *reinterpret_cast<f32x4 *>(rp) = r;
@@ -619,7 +621,9 @@ __global__ __launch_bounds__(256) void split_reduce_kernel(const GemmParams p, c
   f32x4 v = *reinterpret_cast<const f32x4 *>(pp);
   for (int sp = 1; sp < sc.split_s; ++sp) v += *reinterpret_cast<const f32x4 *>(pp + (int64_t)sp * BM * BN);
   float *rp = p.resid + (int64_t)m * p.ldr + n;
-  f32x4 r = p.resid_overwrite ? f32x4{0.f, 0.f, 0.f, 0.f} : *reinterpret_cast<f32x4 *>(rp);
+  f32x4 r = p.resid_overwrite ? f32x4{0.f, 0.f, 0.f, 0.f}
+            : p.resid_in      ? unpack_bf16x4(ld8(p.resid_in + (int64_t)m * p.ldr + n))
+                              : *reinterpret_cast<f32x4 *>(rp);
   r += v;
   *reinterpret_cast<f32x4 *>(rp) = r;
   if (p.resid_out) st8(p.resid_out + (int64_t)m * p.ldr + n, pack_bf16x4(r[0], r[1], r[2], r[3]));

@@ -74,6 +74,10 @@ struct GemmParams {
   int pos0;
   // EPI_RESID: resid[m, n] += acc (= acc when resid_overwrite); resid_out (nullable) = bf16(resid)
   float *resid;
+  // EPI_RESID (nullable): the residual before the update in bf16, same layout
+  // as resid, read instead of resid (the window's first update reads its
+  // boundary state directly, so the fp32 copy of it is never written)
+  const bf16 *resid_in;
   bf16 *resid_out;
   int ldr;
   int resid_overwrite;
