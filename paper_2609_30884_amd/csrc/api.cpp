@@ -464,6 +464,7 @@ crf_status run_layers_bf16(crf_context *ctx, const void *hb, const crf_layer_wei
       }
       p.resid = ctx->hres;
       p.resid_out = (last && hout) ? (bf16 *)hout : nullptr;
+      p.resid_final = p.resid_out && !skinny;  // nothing reads the fp32 residual after the window
       p.ldr = D;
       LAUNCH(ctx, s, CRF_KK_GEMM_DOWN, gemm(EPI_RESID, p));
     }

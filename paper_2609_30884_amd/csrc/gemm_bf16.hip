@@ -435,7 +435,7 @@ __global__ __launch_bounds__(64 * WAVES, 1) void gemm_bf16_kernel(const GemmPara
                                         : *reinterpret_cast<f32x4 *>(rp);
 #pragma unroll
             for (int jj = 0; jj < 4; ++jj) r[jj] += acc[ii][j][q * 4 + jj];
-            *reinterpret_cast<f32x4 *>(rp) = r;
+            if (!p.resid_final) *reinterpret_cast<f32x4 *>(rp) = r;
             if (p.resid_out) st8(p.resid_out + (int64_t)m * p.ldr + n, pack_bf16x4(r[0], r[1], r[2], r[3]));
           }
       }
@@ -625,7 +625,7 @@ __global__ __launch_bounds__(256) void split_reduce_kernel(const GemmParams p, c
             : p.resid_in      ? unpack_bf16x4(ld8(p.resid_in + (int64_t)m * p.ldr + n))
                               : *reinterpret_cast<f32x4 *>(rp);
   r += v;
-  *reinterpret_cast<f32x4 *>(rp) = r;
+  if (!p.resid_final) *reinterpret_cast<f32x4 *>(rp) = r;
   if (p.resid_out) st8(p.resid_out + (int64_t)m * p.ldr + n, pack_bf16x4(r[0], r[1], r[2], r[3]));
 }
 

@@ -79,6 +79,7 @@ struct GemmParams {
   // boundary state directly, so the fp32 copy of it is never written)
   const bf16 *resid_in;
   bf16 *resid_out;
+  int resid_final;  // EPI_RESID with resid_out: the updated residual is stored only as resid_out
   int ldr;
   int resid_overwrite;
   // EPI_SWIGLU: act[m, f] = silu(gate) * up
