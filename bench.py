@@ -138,10 +138,13 @@ def tail_skipped_flops(dims, n, rank, targets):
 
 def hbm_bytes(dims, n, h, rank, targets, kv_tail):
     """Algorithmic HBM bytes per window of the HBM-bound kernel classes (each
-    tensor read or written once): RMSNorm (bf16 or fp32 residual in, bf16 out)
-    and the skinny LoRA-down passes (activation in, rank columns out)."""
+    tensor read or written once): RMSNorm (bf16 or fp32 residual in, bf16 out;
+    the window's first norm of a few rows also writes the fp32 residual copy,
+    which longer windows read from the boundary state instead) and the skinny
+    LoRA-down passes (activation in, rank columns out)."""
     d, dq, f = dims.d_model, dims.dq, dims.d_ffn
-    norm = n * d * (2 + 4 + 2) + (2 * h - 1 - (1 if kv_tail else 0)) * n * d * (4 + 2)
+    first = n * d * (2 + 2) if n > 16 else n * d * (2 + 4 + 2)
+    norm = first + (2 * h - 1 - (1 if kv_tail else 0)) * n * d * (4 + 2)
     r3 = 3 * rank * 2
     per_layer = {"qkv": n * d * 2 + n * r3, "o": n * dq * 2 + n * r3, "gateup": n * d * 2 + n * r3,
                  "down": n * f * 2 + n * r3}
