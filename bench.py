@@ -174,7 +174,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: the recomputation path is built and measured on a single MI355X "
-              f"(--gpus {args.gpus} is not supported; see DESIGN.md for how it would shard).", file=sys.stderr)
+              f"(--gpus {args.gpus} is not supported: no part of it is sharded over GPUs).", file=sys.stderr)
         sys.exit(2)
 
     import torch
