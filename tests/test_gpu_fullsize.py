@@ -23,7 +23,7 @@ import numpy as np
 import pytest
 
 import synthetic as syn
-from tests.helpers import MODEL_HEADROOM, TOL, TOL_ELEM, cdims, rel_to_rms, rms_rel
+from tests.helpers import MODEL_HEADROOM, MODEL_RMS_MATCH, TOL, TOL_ELEM, cdims, rel_to_rms, rms_rel
 
 pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
@@ -118,6 +118,11 @@ def test_full_size_window_whole_tensors():
     print(f"[parity] {name} whole tensors (rms-rel, elem / elem bound) " +
           " ".join(f"{k}=({a:.2e},{b:.2e}/{bounds[k][1]:.2e})" for k, (a, b) in errs.items()), flush=True)
     _check(errs, bounds, name)
+    # the same tensors as the stored model run: the relative RMS errors agree
+    stored = json.load(open(os.path.join(GOLDEN, "bf16_model_errors.json")))[name]["errors"]
+    ratio = {k: errs[k][0] / stored[k]["rms_rel"] for k in errs}
+    print(f"[model] {name} rms-rel gpu/model " + " ".join(f"{k}={v:.3f}" for k, v in ratio.items()), flush=True)
+    assert all(abs(v - 1.0) <= MODEL_RMS_MATCH for v in ratio.values()), ratio
 
 
 def test_full_size_suffix_window():
