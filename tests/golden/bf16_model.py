@@ -54,9 +54,21 @@ def _bf16(x):
     return syn.round_bf16(np.asarray(x, F32))
 
 
+# Deviations from ideal execution that the tests plant to see which of them
+# the parity check on the model's RMS error notices: an extra bf16 rounding of
+# the residual stream after each residual update, or one of the model's
+# rounding points left out (the tensor kept in fp32).
+ROUNDING_POINTS = ("x", "u", "q", "k", "v", "p", "attn", "act")
+VARIANTS = ("resid_bf16",) + tuple("skip_" + r for r in ROUNDING_POINTS)
+
+
 def model_layer(h: np.ndarray, w: Mapping[str, np.ndarray], lora, dims, scale: float = 1.0,
-                rnd: Callable = _bf16, first: bool = True):
-    """One decoder layer as the kernels execute it: returns (H_l fp32, K_l, V_l)."""
+                rnd: Callable = _bf16, first: bool = True, variant: str = ""):
+    """One decoder layer as the kernels execute it: returns (H_l fp32, K_l, V_l).
+    variant: one of VARIANTS, or "" for ideal execution."""
+    assert variant in ("",) + VARIANTS, variant
+    rres = rnd if variant == "resid_bf16" else _ident
+    r_ = {pt: (_ident if variant == "skip_" + pt else rnd) for pt in ROUNDING_POINTS}
     lora = lora or {}
     h = np.asarray(h, F32)
     n = h.shape[0]
@@ -65,13 +77,13 @@ def model_layer(h: np.ndarray, w: Mapping[str, np.ndarray], lora, dims, scale: f
 
     def norm(x, g):
         ms = np.mean(x * x, axis=1, keepdims=True, dtype=F32)
-        return rnd(x * (F32(1.0) / np.sqrt(ms + F32(dims.rms_eps))) * np.asarray(g, F32))
+        return r_["x"](x * (F32(1.0) / np.sqrt(ms + F32(dims.rms_eps))) * np.asarray(g, F32))
 
     def lin(x, t, bias=None):
         y = x @ np.asarray(w["w_" + t], F32).T
         if t in lora:
             a, b = lora[t]
-            u = rnd(F32(scale) * (x @ np.asarray(a, F32).T))
+            u = r_["u"](F32(scale) * (x @ np.asarray(a, F32).T))
             y = y + u @ np.asarray(b, F32).T
         if bias is not None:
             y = y + np.asarray(bias, F32)
@@ -87,9 +99,9 @@ def model_layer(h: np.ndarray, w: Mapping[str, np.ndarray], lora, dims, scale: f
 
     x = norm(h, w["attn_norm"])
     c2 = F32(1.4426950408889634 / math.sqrt(hd))
-    q = rnd(rope(lin(x, "q", w.get("bias_q")).reshape(n, nq, hd)) * c2)
-    k = rnd(rope(lin(x, "k", w.get("bias_k")).reshape(n, nkv, hd)))
-    v = rnd(lin(x, "v", w.get("bias_v")).reshape(n, nkv, hd))
+    q = r_["q"](rope(lin(x, "q", w.get("bias_q")).reshape(n, nq, hd)) * c2)
+    k = r_["k"](rope(lin(x, "k", w.get("bias_k")).reshape(n, nkv, hd)))
+    v = r_["v"](lin(x, "v", w.get("bias_v")).reshape(n, nkv, hd))
     o = np.empty((n, nq, hd), F32)
     rep = nq // nkv
     blk = 512
@@ -102,13 +114,13 @@ def model_layer(h: np.ndarray, w: Mapping[str, np.ndarray], lora, dims, scale: f
             s[mask] = -np.inf
             p = np.exp2(s - s.max(axis=1, keepdims=True))
             l_ = p.sum(axis=1, keepdims=True, dtype=F32)
-            o[a0:b0, j, :] = (rnd(p) @ v[:b0, g, :]) / l_
-    attn = rnd(o.reshape(n, nq * hd))
-    h = h + lin(attn, "o")
+            o[a0:b0, j, :] = (r_["p"](p) @ v[:b0, g, :]) / l_
+    attn = r_["attn"](o.reshape(n, nq * hd))
+    h = rres(h + lin(attn, "o"))
     x2 = norm(h, w["mlp_norm"])
     gt, up = lin(x2, "gate"), lin(x2, "up")
-    act = rnd(gt / (F32(1.0) + np.exp(-gt)) * up)
-    h = h + lin(act, "down")
+    act = r_["act"](gt / (F32(1.0) + np.exp(-gt)) * up)
+    h = rres(h + lin(act, "down"))
     return h, k, v
 
 
@@ -122,9 +134,9 @@ def errors(got: np.ndarray, ref: np.ndarray) -> Tuple[float, float]:
 
 
 def window_errors(wl: syn.Workload, item: int = 0, seed: int = SEED, rnd: Callable = _bf16,
-                  n_tokens: Optional[int] = None, log=None) -> Dict[str, Tuple[float, float]]:
+                  n_tokens: Optional[int] = None, log=None, variant: str = "") -> Dict[str, Tuple[float, float]]:
     """Model vs oracle errors for one window of a workload (optionally on the
-    first n_tokens of its prefix)."""
+    first n_tokens of its prefix, optionally with a planted deviation)."""
     win = wl.windows[item]
     n = win.n_tokens if n_tokens is None else n_tokens
     dims = wl.dims
@@ -138,7 +150,7 @@ def window_errors(wl: syn.Workload, item: int = 0, seed: int = SEED, rnd: Callab
         t0 = time.perf_counter()
         ref, kr, vr = O.decoder_layer(ref, w, lo, dims, wl.lora_scale)
         t1 = time.perf_counter()
-        cur, km, vm = model_layer(cur, w, lo, dims, wl.lora_scale, rnd)
+        cur, km, vm = model_layer(cur, w, lo, dims, wl.lora_scale, rnd, variant=variant)
         out[f"K{l}"] = errors(km, kr)
         out[f"V{l}"] = errors(vm, vr)
         if log:

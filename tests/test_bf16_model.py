@@ -73,3 +73,22 @@ def test_stored_run_reproduces():
     for k, (a, b) in e.items():
         assert a == pytest.approx(stored[k]["rms_rel"], rel=2e-2)
         assert b == pytest.approx(stored[k]["elem"], rel=5e-2)
+
+
+def test_model_rms_match_notices_planted_deviations():
+    """The GPU tests require the GPU's relative RMS error to equal the model's to
+    within MODEL_RMS_MATCH.  Planted in the model, an extra bf16 rounding of the
+    residual stream after each update, or a missing rounding of the normalised
+    inputs or of the stored K or V (the dominant terms), moves that ratio past
+    it on some tensor; the other rounding points (U, Q, P, the attention and
+    SwiGLU outputs) weigh too little in these errors for the check to see them."""
+    from tests.helpers import MODEL_RMS_MATCH
+    wl = _small(h=2)
+    base = M.window_errors(wl)
+    for variant in ("resid_bf16", "skip_x", "skip_k", "skip_v"):
+        e = M.window_errors(wl, variant=variant)
+        worst = max(abs(e[k][0] / base[k][0] - 1.0) for k in base)
+        assert worst > 3 * MODEL_RMS_MATCH, (variant, worst)
+    for variant in M.VARIANTS:  # every planted deviation keeps the window bf16-sized
+        e = M.window_errors(wl, variant=variant)
+        assert max(a for a, _ in e.values()) < TOL["bf16"]
