@@ -689,20 +689,38 @@ __global__ __launch_bounds__(256) void qkv_split_reduce_kernel(const GemmParams 
 // U[m, ucol + r] = bf16(scale * sum of the fused down-projection adapter sums
 // of token m): over the runs that cover m's token tile in increasing order of
 // their first tile, then over the two feature halves.  One thread per 4 ranks.
+constexpr int DN_MAX_TILES_N = 1024;  // feature tiles of a gate/up row the slot list holds (d_ffn <= 131072)
+
 __global__ __launch_bounds__(256) void dn_sum_kernel(const GemmParams p, const Sched sc, bf16 *U, int ldu, int ucol,
                                                      float scale) {
+  // the workgroup's 64 tokens share one token tile: its slots, in order of
+  // their first feature tile, are listed once in LDS (wave 0 compacts the
+  // table with ballots), then every thread walks the short list
+  __shared__ int slots[DN_MAX_TILES_N];
+  __shared__ int n_slots;
   const int idx = blockIdx.x * 256 + threadIdx.x;
   const int m = idx / (DN_RANK / 4), r = 4 * (idx % (DN_RANK / 4));
+  const int tm = (blockIdx.x * 256 / (DN_RANK / 4)) / BM, ml = m % BM;
+  if (threadIdx.x < 64) {
+    const int *head = p.dn_head + tm * sc.tiles_n;
+    int count = 0;
+    for (int t0 = 0; t0 < sc.tiles_n; t0 += 64) {
+      const int tn = t0 + (int)threadIdx.x;
+      const int h = tn < sc.tiles_n ? head[tn] : 0;
+      const uint64_t mask = __ballot(h != 0);
+      if (h) slots[count + __popcll(mask & ((1ull << threadIdx.x) - 1))] = h - 1;
+      count += __popcll(mask);
+    }
+    if (threadIdx.x == 0) n_slots = count;
+  }
+  __syncthreads();
   if (m >= p.M || r >= p.dn_rank) return;
-  const int tm = m / BM, ml = m % BM;
-  const int *head = p.dn_head + tm * sc.tiles_n;
   f32x4 v = {0.f, 0.f, 0.f, 0.f};
-  for (int tn = 0; tn < sc.tiles_n; ++tn) {
-    const int h = head[tn];
-    if (!h) continue;
+  for (int i = 0; i < n_slots; ++i) {
+    const int slot = slots[i];
 #pragma unroll
     for (int wn = 0; wn < 2; ++wn)
-      v += *reinterpret_cast<const f32x4 *>(p.dn_part + (((int64_t)(h - 1) * 2 + wn) * BM + ml) * DN_RANK + r);
+      v += *reinterpret_cast<const f32x4 *>(p.dn_part + (((int64_t)slot * 2 + wn) * BM + ml) * DN_RANK + r);
   }
   bf16 *u = U + (int64_t)m * ldu + ucol + r;
 #pragma unroll
@@ -755,7 +773,7 @@ hipError_t go(hipStream_t s, const GemmParams &p0, bool *dn_done) {
   p.split_s = sc.split_s;
   bool dn = false;
   if (EPI == EPI_SWIGLU && p.dn_a && p.dn_part && p.dn_head && p.dn_rank > 0 && p.dn_rank <= DN_RANK &&
-      p.dn_runs > 0 && STAGE_BYTES + DN_BYTES <= 160 * 1024) {
+      p.dn_runs > 0 && STAGE_BYTES + DN_BYTES <= 160 * 1024 && sc.tiles_n <= DN_MAX_TILES_N) {
     int runs = 0;
     for (int b = 0; b < sc.grid && runs <= p.dn_runs; ++b) runs = std::max(runs, n_runs(sc, b));
     dn = runs <= p.dn_runs;
@@ -810,6 +828,7 @@ hipError_t launch_gemm_dn_sum(hipStream_t s, const GemmParams &p, bf16 *U, int l
   if (p.M <= 0) return hipSuccess;
   const Sched sc = schedule(EPI_SWIGLU, p);
   const int threads = p.M * (DN_RANK / 4);
+  if (sc.tiles_n > DN_MAX_TILES_N) return hipErrorInvalidValue;
   hipLaunchKernelGGL(dn_sum_kernel, dim3((threads + 255) / 256), dim3(256), 0, s, p, sc, U, ldu, ucol, scale);
   return hipGetLastError();
 }
