@@ -97,8 +97,45 @@ struct PageMap {
   }
 };
 
+// Query head and query block of workgroup `bid` over nqb blocks of BQ rows;
+// false for padding at the end of a per-XCD list (uniform per workgroup).
+// Packed: one workgroup per KV head carries the group's query heads stacked on
+// the rows of one tile.  xcd_r > 0: XCD x (= bid % 8) serves KV head x / xcd_r
+// and every xcd_r-th query block from x % xcd_r, longest causal rows first,
+// with the group's query heads adjacent.  Otherwise head-major, longest rows
+// first.
+__host__ __device__ inline bool attn_block(int bid, int nq, int nkv, int nqb, int xcd_r, int packed, int &head,
+                                           int &qblk) {
+  const int group = nq / nkv;
+  if (packed) {
+    head = bid * group;
+    qblk = 0;
+    return true;
+  }
+  if (xcd_r > 0) {
+    const int x = bid % 8, j = bid / 8;
+    const int qi = j / group;
+    head = (x / xcd_r) * group + j % group;
+    qblk = nqb - 1 - (qi * xcd_r + x % xcd_r);
+    return qblk >= 0;
+  }
+  head = bid % nq;
+  qblk = nqb - 1 - bid / nq;
+  return true;
+}
+
+// Workgroups of a window launch (no key split); sets xcd_r for attn_block
+// (0 when the KV-head count does not divide the XCD count).
+inline int attn_window_grid(int nq, int nkv, int nqb, int &xcd_r) {
+  if (nkv <= 8 && 8 % nkv == 0) {
+    xcd_r = 8 / nkv;
+    return 8 * (nq / nkv) * ((nqb + xcd_r - 1) / xcd_r);
+  }
+  xcd_r = 0;
+  return nqb * nq;
+}
+
 // PS: page size when fixed at compile time (16), 0 = runtime kv.page_size.
-// XCD: balanced per-XCD KV-head mapping (R = 8 / nkv XCDs per KV head).
 template <int HD, int PS>
 __global__ __launch_bounds__(NT, 8 / NW) void attn_bf16_kernel(const bf16 *__restrict__ Q, PagedKV kv,
                                                            bf16 *__restrict__ O, int Mq, int q_off, int nq,
@@ -123,19 +160,7 @@ __global__ __launch_bounds__(NT, 8 / NW) void attn_bf16_kernel(const bf16 *__res
   const int nqb = (Mq + BQ - 1) / BQ;
   const int group = nq / nkv;
   int head, qblk;
-  if (packed) {  // the group's query heads stacked on the rows of one tile
-    head = blockIdx.x * group;
-    qblk = 0;
-  } else if (xcd_r > 0) {
-    const int x = blockIdx.x % 8, j = blockIdx.x / 8;
-    const int qi = j / group;
-    head = (x / xcd_r) * group + j % group;
-    qblk = nqb - 1 - (qi * xcd_r + x % xcd_r);
-    if (qblk < 0) return;  // padding of the per-XCD lists (uniform per workgroup)
-  } else {
-    head = blockIdx.x % nq;
-    qblk = nqb - 1 - blockIdx.x / nq;  // longest causal rows first
-  }
+  if (!attn_block(blockIdx.x, nq, nkv, nqb, xcd_r, packed, head, qblk)) return;
   const int g_kv = head / group;
   const int ps = PS > 0 ? PS : kv.page_size;
   const int tid = threadIdx.x, lane = tid % 64;
@@ -478,9 +503,8 @@ void launch(hipStream_t s, const bf16 *Q, const PagedKV &kv, bf16 *O, int Mq, in
     split_tiles = std::max<int>(split_tiles, (int)((ntiles + max_splits - 1) / max_splits));
     n_splits = (ntiles + split_tiles - 1) / split_tiles;
     grid = units;
-  } else if (nkv <= 8 && 8 % nkv == 0) {
-    xcd_r = 8 / nkv;
-    grid = 8 * (nq / nkv) * ((nqb + xcd_r - 1) / xcd_r);
+  } else {
+    grid = attn_window_grid(nq, nkv, nqb, xcd_r);
   }
   const dim3 g3(grid, n_splits);
   if (kv.page_size == 16)
